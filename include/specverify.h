@@ -1,0 +1,194 @@
+/*
+ * specverify: one batched speculative-decoding tree-verify step on an
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (RLHFSpec, Section 2.2 "Speculative Decoding"; Section 5.2
+ * names its two costs, attention over the KV cache and the FFN matrix
+ * products; Section 6.2 fixes that a step never rewrites verified KV):
+ *
+ *   For every live sample b the caller hands in a committed KV length S_b
+ *   and a draft token tree of T_b nodes (node 0 = root = the token decided
+ *   by the previous step, whose K/V are not cached yet).  The target model,
+ *   a Llama-style decoder, runs one forward pass over all N = sum T_b
+ *   nodes: node i sits at position S_b + depth(i) and attends to the whole
+ *   committed prefix plus its own ancestors in the tree (itself included).
+ *   Greedy acceptance then takes g_i = argmax of node i's logits (lowest
+ *   token id on ties), accepts a node when every edge on its branch carries
+ *   the token its parent predicted (the root is always accepted), and
+ *   picks the deepest accepted node (lowest node index on ties):
+ *   accepted_len = its depth, next_token = its g.  Committing moves the K/V
+ *   of the accepted branch to cache positions S_b .. S_b + accepted_len and
+ *   the committed length becomes S_b + accepted_len + 1.
+ *
+ * Conventions for every entry point:
+ *   - Return value: SPEC_OK (0) or a negative spec_status.  On a validation
+ *     failure nothing has been enqueued and no output or KV byte has been
+ *     written; spec_last_error() then describes the failure.
+ *   - Work is enqueued on the caller's HIP stream (passed as void*; NULL is
+ *     the null stream) and is asynchronous: device outputs are valid once
+ *     the stream has been synchronised.
+ *   - "host" / "device" below says where a pointer must point.  All device
+ *     memory (weights, KV pool, workspace, outputs) is allocated and owned
+ *     by the caller; the library never allocates device memory.  The only
+ *     allocations it makes are its opaque handle and a small pinned host
+ *     staging area inside it.
+ *   - One spec_kv handle must not be used from two threads or two streams
+ *     at once.
+ *   - Numerics: bf16 weights, bf16 activations at GEMM inputs, bf16 KV
+ *     cache; fp32 accumulation, softmax, norms and residual stream.
+ *   - Supported shapes: head_dim 64 or 128; hidden, n_heads*head_dim and
+ *     ffn multiples of 128; n_kv_heads*head_dim a multiple of 128; vocab a
+ *     multiple of 128; n_heads a multiple of n_kv_heads; 1 <= T_b <=
+ *     SPEC_MAX_TREE.  Anything else returns SPEC_ERR_UNSUPPORTED.
+ */
+#ifndef SPECVERIFY_H
+#define SPECVERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPEC_MAX_TREE 64
+
+typedef enum {
+  SPEC_OK = 0,
+  SPEC_ERR_INVALID = -1,     /* null pointer, non-positive size, bad config or sample id */
+  SPEC_ERR_TREE = -2,        /* parents[0] != -1, parent not before child, token out of range */
+  SPEC_ERR_CAPACITY = -3,    /* S_b + T_b exceeds the sample's KV capacity, or buffer too small */
+  SPEC_ERR_WORKSPACE = -5,   /* workspace smaller than the call needs */
+  SPEC_ERR_UNSUPPORTED = -6, /* shape outside the supported set (see above) */
+  SPEC_ERR_HIP = -7          /* a HIP runtime call or kernel launch failed */
+} spec_status;
+
+/* Llama-style decoder shape.  rope_theta: base of the rotary frequencies,
+ * frequency j = rope_theta^(-2j/head_dim), half-split rotation (element j
+ * pairs with j + head_dim/2).  rms_eps: RMSNorm epsilon. */
+typedef struct {
+  int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
+  float rope_theta, rms_eps;
+} spec_model_config;
+
+/* Weights: device pointers to row-major bf16 matrices in [out][in] layout
+ * (a GEMM computes x . W^T), read-only, owned by the caller.  The per-layer
+ * fields are HOST arrays of n_layers device pointers. */
+typedef struct {
+  const void* tok_embed;        /* [vocab][hidden] */
+  const void* final_norm;       /* [hidden] RMSNorm gain */
+  const void* lm_head;          /* [vocab][hidden] (untied) */
+  const void* const* attn_norm; /* [hidden] */
+  const void* const* wq;        /* [n_heads*head_dim][hidden] */
+  const void* const* wk;        /* [n_kv_heads*head_dim][hidden] */
+  const void* const* wv;        /* [n_kv_heads*head_dim][hidden] */
+  const void* const* wo;        /* [hidden][n_heads*head_dim] */
+  const void* const* ffn_norm;  /* [hidden] */
+  const void* const* w_gate;    /* [ffn][hidden] */
+  const void* const* w_up;      /* [ffn][hidden] */
+  const void* const* w_down;    /* [hidden][ffn] */
+} spec_weights;
+
+/* Opaque KV-pool handle (host memory, owned by the library). */
+typedef struct spec_kv spec_kv;
+
+/* Optional device dumps for tests; any field may be NULL.  N = sum T_b,
+ * rows in batch order (sample 0's nodes first, each tree in its own node
+ * order). */
+typedef struct {
+  float* logits;      /* [N][vocab] fp32 */
+  int32_t* argmax;    /* [N] greedy token after each node */
+  int32_t* depth;     /* [N] depth of each node (root 0) */
+  int32_t* pos;       /* [N] position S_b + depth */
+  uint64_t* anc;      /* [N] ancestor set, bit t = node t of the same tree, own bit set */
+} spec_debug;
+
+/* ---- KV pool (Section 6.2: verified KV is never rewritten) -------------
+ *
+ * Layout: sample s owns one contiguous block of
+ *   n_layers * 2 * n_kv_heads * capacity[s] * head_dim  bf16 values,
+ * ordered [layer][K=0,V=1][kv_head][position][head_dim]; blocks follow each
+ * other in sample order, each starting at a 256-byte aligned offset.
+ * Positions [0, S_s) hold committed K/V (K already rotated). */
+
+/* Bytes a pool for n_samples samples with the given host capacities needs,
+ * or 0 if an argument is invalid. */
+size_t spec_kv_bytes(const spec_model_config* cfg, int32_t n_samples, const int32_t* capacity);
+
+/* Create a handle over caller memory device_buf (device, >= spec_kv_bytes,
+ * 256-byte aligned).  capacity: host [n_samples].  *out receives the handle. */
+int spec_kv_alloc(const spec_model_config* cfg, int32_t n_samples, const int32_t* capacity,
+                  void* device_buf, size_t buf_bytes, spec_kv** out);
+
+/* Release the handle (not device_buf).  Waits for the handle's pending
+ * staging copies. */
+int spec_kv_free(spec_kv* kv);
+
+/* Byte offset of sample's block inside device_buf and its capacity. */
+int spec_kv_sample_layout(const spec_kv* kv, int32_t sample, int64_t* byte_offset,
+                          int32_t* capacity);
+
+/* ---- The verify step ---------------------------------------------------- */
+
+/* Workspace bytes spec_verify needs for up to max_batch samples and
+ * max_tokens tree nodes in total; 0 if an argument is invalid. */
+size_t spec_workspace_bytes(const spec_model_config* cfg, int32_t max_batch, int32_t max_tokens);
+
+/* One tree-verify step over `batch` live samples.
+ *   sample_ids   host [batch]   pool sample of each live sample (distinct)
+ *   tree_offsets host [batch+1] tree_offsets[0] = 0, T_b = diff, 1..SPEC_MAX_TREE
+ *   tree_tokens  host [N]       token of every node, in [0, vocab)
+ *   tree_parents host [N]       parent node index within the same tree;
+ *                               -1 for node 0, 0 <= parent < node otherwise
+ *   seq_lens     host [batch]   committed length S_b, S_b + T_b <= capacity
+ *   workspace    device, ws_bytes >= spec_workspace_bytes(cfg, batch, N)
+ * Outputs (device, int32):
+ *   accepted_len   [batch]                  depth of the deepest accepted node
+ *   next_token     [batch]                  greedy token after that node
+ *   accepted_nodes [batch][SPEC_MAX_TREE]   node ids of the accepted branch,
+ *                                           root first, then -1
+ * KV effect: writes the nodes' K/V to positions S_b + node of each sample
+ * (never below S_b).  dbg may be NULL. */
+int spec_verify(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv,
+                int32_t batch, const int32_t* sample_ids, const int32_t* tree_offsets,
+                const int32_t* tree_tokens, const int32_t* tree_parents, const int32_t* seq_lens,
+                void* workspace, size_t ws_bytes, void* stream,
+                int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
+                const spec_debug* dbg);
+
+/* Commit the accepted branches of the preceding spec_verify (same batch,
+ * sample_ids and seq_lens, same stream): the K/V of node accepted_nodes[b][d]
+ * moves to position S_b + d for d = 1..accepted_len[b] (all layers, K and
+ * V), and new_seq_lens[b] = S_b + accepted_len[b] + 1.
+ *   accepted_len, accepted_nodes: device, as written by spec_verify
+ *   new_seq_lens: device [batch] int32 output */
+int spec_kv_commit(spec_kv* kv, int32_t batch, const int32_t* sample_ids,
+                   const int32_t* seq_lens, const int32_t* accepted_len,
+                   const int32_t* accepted_nodes, int32_t* new_seq_lens, void* stream);
+
+/* Message of the last failure on the calling thread ("" if none). */
+const char* spec_last_error(void);
+
+/* ---- Kernel timing (measurement only) ----------------------------------
+ * While enabled, every launch of the named kernel class is bracketed by a
+ * pair of HIP events on its stream.  spec_profile_end synchronises those
+ * events, returns the summed duration in ms and the launch count, and
+ * disables timing.  Kernel classes: */
+enum {
+  SPEC_K_GEMM_QKV = 0,
+  SPEC_K_ATTENTION = 1,
+  SPEC_K_GEMM_O = 2,
+  SPEC_K_GEMM_GATE_UP = 3,
+  SPEC_K_GEMM_DOWN = 4,
+  SPEC_K_LM_HEAD = 5,
+  SPEC_K_COMMIT = 6,
+  SPEC_K_COUNT = 7
+};
+int spec_profile_begin(int32_t kernel_class, int32_t max_launches);
+int spec_profile_end(float* total_ms, int32_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECVERIFY_H */

@@ -1,0 +1,25 @@
+"""MI355X-native batched speculative-decoding tree-verify step.
+
+The computation lives in the HIP library libspecverify.so (C ABI declared in
+include/specverify.h); this package is its Python binding.  The library is
+loaded on first use and its absence is an error.
+"""
+
+from .binding import (  # noqa: F401
+    EXPORTS,
+    KVPool,
+    SPEC_MAX_TREE,
+    SpecError,
+    Weights,
+    lib,
+    spec_kv_alloc,
+    spec_kv_bytes,
+    spec_kv_commit,
+    spec_kv_free,
+    spec_kv_sample_layout,
+    spec_profile_begin,
+    spec_profile_end,
+    spec_verify,
+    spec_workspace_bytes,
+)
+from .session import Verifier, flatten_trees  # noqa: F401

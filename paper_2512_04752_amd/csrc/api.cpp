@@ -1,0 +1,562 @@
+// Host side of the specverify C ABI: argument validation, per-call planning
+// (per-sample descriptors, split-KV attention work list), workspace carving,
+// one staged host-to-device upload per call and the launch sequence of the
+// verify step.  Every step of the computation itself runs in the HIP kernels.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "specverify.h"
+
+#define SPEC_API extern "C" __attribute__((visibility("default")))
+
+using namespace spec;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(SPEC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)               \
+  do {                                    \
+    hipError_t e_ = (expr);               \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr int kPartCap = 8192;          // split-KV partial tiles per call
+constexpr int kTargetItems = 2048;      // attention work-groups aimed for
+constexpr int kMinChunk = 256;          // keys per split, lower bound
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool config_ok(const spec_model_config* c, std::string* why) {
+  char buf[256];
+  auto bad = [&](const char* m) {
+    snprintf(buf, sizeof buf, "unsupported model shape: %s", m);
+    *why = buf;
+    return false;
+  };
+  if (c->n_layers < 1 || c->hidden < 1 || c->n_heads < 1 || c->n_kv_heads < 1 || c->ffn < 1 ||
+      c->vocab < 1 || c->head_dim < 1)
+    return bad("non-positive dimension");
+  if (c->head_dim != 64 && c->head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c->n_heads % c->n_kv_heads) return bad("n_heads must be a multiple of n_kv_heads");
+  if (c->hidden % 128) return bad("hidden must be a multiple of 128");
+  if ((c->n_heads * c->head_dim) % 128) return bad("n_heads*head_dim must be a multiple of 128");
+  if ((c->n_kv_heads * c->head_dim) % 128)
+    return bad("n_kv_heads*head_dim must be a multiple of 128");
+  if (c->ffn % 128) return bad("ffn must be a multiple of 128");
+  if (c->vocab % 128) return bad("vocab must be a multiple of 128");
+  if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return bad("rope_theta/rms_eps");
+  return true;
+}
+
+bool same_config(const spec_model_config* a, const spec_model_config* b) {
+  return a->n_layers == b->n_layers && a->hidden == b->hidden && a->n_heads == b->n_heads &&
+         a->n_kv_heads == b->n_kv_heads && a->head_dim == b->head_dim && a->ffn == b->ffn &&
+         a->vocab == b->vocab;
+}
+
+size_t sample_bytes(const spec_model_config* c, int32_t cap) {
+  return align_up((size_t)c->n_layers * 2 * c->n_kv_heads * (size_t)cap * c->head_dim * 2);
+}
+
+// Workspace carving; every region 256-byte aligned.
+struct WsLayout {
+  size_t blob, toks, anc, rope, x, h, q, o, act, part_o, part_ml, lm_val, lm_idx, argmax, total;
+  size_t blob_bytes;
+};
+
+int64_t max_row_tiles(const spec_model_config* c, int64_t max_batch, int64_t max_tokens) {
+  const int64_t G = c->n_heads / c->n_kv_heads;
+  return (int64_t)c->n_kv_heads * ((max_tokens * G + 31) / 32 + max_batch);
+}
+
+WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_tokens) {
+  WsLayout L{};
+  const int64_t items = max_row_tiles(c, max_batch, max_tokens) + kPartCap;
+  L.blob_bytes = align_up(max_batch * sizeof(SampleInfo)) + 2 * align_up(max_tokens * 4) +
+                 align_up(items * sizeof(AttnItem)) + align_up(kPartCap * sizeof(CombineItem));
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes);
+    return at;
+  };
+  const size_t nq_hd = (size_t)c->n_heads * c->head_dim;
+  L.blob = take(L.blob_bytes);
+  L.toks = take(max_tokens * sizeof(TokInfo));
+  L.anc = take(max_tokens * 8);
+  L.rope = take(max_tokens * (size_t)(c->head_dim / 2) * 8);
+  L.x = take(max_tokens * (size_t)c->hidden * 4);
+  L.h = take(max_tokens * (size_t)c->hidden * 2);
+  L.q = take(max_tokens * nq_hd * 2);
+  L.o = take(max_tokens * nq_hd * 2);
+  L.act = take(max_tokens * (size_t)c->ffn * 2);
+  L.part_o = take((size_t)kPartCap * 32 * c->head_dim * 4);
+  L.part_ml = take((size_t)kPartCap * 32 * 2 * 4);
+  L.lm_val = take(max_tokens * (size_t)(c->vocab / 64) * 4);
+  L.lm_idx = take(max_tokens * (size_t)(c->vocab / 64) * 4);
+  L.argmax = take(max_tokens * 4);
+  L.total = off;
+  return L;
+}
+
+// Process-wide kernel timing state (measurement only).
+struct Profiler {
+  bool on = false;
+  int kind = -1, max = 0, count = 0;
+  std::vector<hipEvent_t> ev;
+} g_prof;
+
+template <class F>
+hipError_t timed(int kind, hipStream_t s, F&& fn) {
+  const bool rec = g_prof.on && g_prof.kind == kind && g_prof.count < g_prof.max;
+  if (rec) {
+    const hipError_t e = hipEventRecord(g_prof.ev[2 * g_prof.count], s);
+    if (e != hipSuccess) return e;
+  }
+  const hipError_t e = fn();
+  if (rec) {
+    const hipError_t e2 = hipEventRecord(g_prof.ev[2 * g_prof.count + 1], s);
+    ++g_prof.count;
+    if (e2 != hipSuccess) return e2;
+  }
+  return e;
+}
+
+}  // namespace
+
+// Library-owned part of a KV pool: capacities, block offsets and a two-slot
+// pinned staging ring for the per-call host->device uploads.
+struct spec_kv {
+  spec_model_config cfg;
+  int32_t n = 0;
+  std::vector<int32_t> cap;
+  std::vector<int64_t> base;     // element offsets of the sample blocks
+  bf16* pool = nullptr;
+  size_t bytes = 0;
+  size_t ctl_off = 0;            // byte offset of the control area (commit descriptors)
+  struct Slot {
+    void* host = nullptr;
+    size_t size = 0;
+    hipEvent_t ev = nullptr;
+    bool pending = false;
+  } slots[2];
+  int next = 0;
+};
+
+namespace {
+
+// Copy `bytes` of `src` to device `dst` through the next pinned staging slot.
+int stage_upload(spec_kv* kv, const void* src, size_t bytes, void* dst, hipStream_t s) {
+  spec_kv::Slot& sl = kv->slots[kv->next];
+  kv->next ^= 1;
+  if (sl.pending) {
+    HIP_TRY(hipEventSynchronize(sl.ev), "staging wait");
+    sl.pending = false;
+  }
+  if (sl.ev == nullptr) HIP_TRY(hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming), "event");
+  if (sl.size < bytes) {
+    if (sl.host) HIP_TRY(hipHostFree(sl.host), "free staging");
+    sl.host = nullptr;
+    sl.size = 0;
+    const size_t want = std::max(bytes, (size_t)1 << 20);
+    HIP_TRY(hipHostMalloc(&sl.host, want, hipHostMallocDefault), "pinned staging");
+    sl.size = want;
+  }
+  memcpy(sl.host, src, bytes);
+  HIP_TRY(hipMemcpyAsync(dst, sl.host, bytes, hipMemcpyHostToDevice, s), "upload");
+  HIP_TRY(hipEventRecord(sl.ev, s), "staging event");
+  sl.pending = true;
+  return SPEC_OK;
+}
+
+int check_samples(const spec_kv* kv, int32_t batch, const int32_t* ids) {
+  std::vector<char> seen(kv->n, 0);
+  for (int b = 0; b < batch; ++b) {
+    const int id = ids[b];
+    if (id < 0 || id >= kv->n) return fail(SPEC_ERR_INVALID, "sample_ids[%d] = %d out of range", b, id);
+    if (seen[id]) return fail(SPEC_ERR_INVALID, "sample id %d appears twice", id);
+    seen[id] = 1;
+  }
+  return SPEC_OK;
+}
+
+}  // namespace
+
+SPEC_API const char* spec_last_error(void) { return g_err.c_str(); }
+
+SPEC_API size_t spec_kv_bytes(const spec_model_config* cfg, int32_t n_samples,
+                              const int32_t* capacity) {
+  std::string why;
+  if (!cfg || !capacity || n_samples < 1 || !config_ok(cfg, &why)) return 0;
+  size_t total = 0;
+  for (int i = 0; i < n_samples; ++i) {
+    if (capacity[i] < 1) return 0;
+    total += sample_bytes(cfg, capacity[i]);
+  }
+  return total + align_up((size_t)n_samples * sizeof(SampleInfo));
+}
+
+SPEC_API int spec_kv_alloc(const spec_model_config* cfg, int32_t n_samples,
+                           const int32_t* capacity, void* device_buf, size_t buf_bytes,
+                           spec_kv** out) {
+  g_err.clear();
+  if (!cfg || !capacity || !device_buf || !out) return fail(SPEC_ERR_INVALID, "null argument");
+  if (n_samples < 1) return fail(SPEC_ERR_INVALID, "n_samples must be >= 1");
+  std::string why;
+  if (!config_ok(cfg, &why)) return fail(SPEC_ERR_UNSUPPORTED, "%s", why.c_str());
+  if ((uintptr_t)device_buf % kAlign) return fail(SPEC_ERR_INVALID, "device_buf not 256-byte aligned");
+  for (int i = 0; i < n_samples; ++i)
+    if (capacity[i] < 1) return fail(SPEC_ERR_INVALID, "capacity[%d] = %d", i, capacity[i]);
+  const size_t need = spec_kv_bytes(cfg, n_samples, capacity);
+  if (buf_bytes < need)
+    return fail(SPEC_ERR_CAPACITY, "KV buffer holds %zu bytes, needs %zu", buf_bytes, need);
+  spec_kv* kv = new spec_kv;
+  kv->cfg = *cfg;
+  kv->n = n_samples;
+  kv->cap.assign(capacity, capacity + n_samples);
+  kv->base.resize(n_samples);
+  size_t off = 0;
+  for (int i = 0; i < n_samples; ++i) {
+    kv->base[i] = (int64_t)(off / 2);
+    off += sample_bytes(cfg, capacity[i]);
+  }
+  kv->ctl_off = off;
+  kv->pool = (bf16*)device_buf;
+  kv->bytes = buf_bytes;
+  *out = kv;
+  return SPEC_OK;
+}
+
+SPEC_API int spec_kv_free(spec_kv* kv) {
+  if (!kv) return fail(SPEC_ERR_INVALID, "null handle");
+  int rc = SPEC_OK;
+  for (auto& sl : kv->slots) {
+    if (sl.pending && hipEventSynchronize(sl.ev) != hipSuccess) rc = SPEC_ERR_HIP;
+    if (sl.ev) (void)hipEventDestroy(sl.ev);
+    if (sl.host) (void)hipHostFree(sl.host);
+  }
+  delete kv;
+  return rc;
+}
+
+SPEC_API int spec_kv_sample_layout(const spec_kv* kv, int32_t sample, int64_t* byte_offset,
+                                   int32_t* capacity) {
+  if (!kv || !byte_offset || !capacity) return fail(SPEC_ERR_INVALID, "null argument");
+  if (sample < 0 || sample >= kv->n) return fail(SPEC_ERR_INVALID, "sample %d out of range", sample);
+  *byte_offset = kv->base[sample] * 2;
+  *capacity = kv->cap[sample];
+  return SPEC_OK;
+}
+
+SPEC_API size_t spec_workspace_bytes(const spec_model_config* cfg, int32_t max_batch,
+                                     int32_t max_tokens) {
+  std::string why;
+  if (!cfg || max_batch < 1 || max_tokens < max_batch || !config_ok(cfg, &why)) return 0;
+  return ws_layout(cfg, max_batch, max_tokens).total;
+}
+
+SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv,
+                         int32_t batch, const int32_t* sample_ids, const int32_t* tree_offsets,
+                         const int32_t* tree_tokens, const int32_t* tree_parents,
+                         const int32_t* seq_lens, void* workspace, size_t ws_bytes, void* stream,
+                         int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
+                         const spec_debug* dbg) {
+  g_err.clear();
+  // ---- validation (no side effects) ----
+  if (!cfg || !w || !kv || !sample_ids || !tree_offsets || !tree_tokens || !tree_parents ||
+      !seq_lens || !workspace || !accepted_len || !next_token || !accepted_nodes)
+    return fail(SPEC_ERR_INVALID, "null argument");
+  std::string why;
+  if (!config_ok(cfg, &why)) return fail(SPEC_ERR_UNSUPPORTED, "%s", why.c_str());
+  if (!same_config(cfg, &kv->cfg)) return fail(SPEC_ERR_INVALID, "config differs from the KV pool's");
+  if (batch < 1) return fail(SPEC_ERR_INVALID, "batch must be >= 1");
+  if (!w->tok_embed || !w->final_norm || !w->lm_head || !w->attn_norm || !w->wq || !w->wk ||
+      !w->wv || !w->wo || !w->ffn_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return fail(SPEC_ERR_INVALID, "null weight pointer");
+  for (int l = 0; l < cfg->n_layers; ++l)
+    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->ffn_norm[l] ||
+        !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
+      return fail(SPEC_ERR_INVALID, "null weight pointer in layer %d", l);
+  if (int rc = check_samples(kv, batch, sample_ids)) return rc;
+  if (tree_offsets[0] != 0) return fail(SPEC_ERR_TREE, "tree_offsets[0] must be 0");
+  for (int b = 0; b < batch; ++b) {
+    const int T = tree_offsets[b + 1] - tree_offsets[b];
+    if (T < 1 || T > SPEC_MAX_TREE)
+      return fail(T < 1 ? SPEC_ERR_TREE : SPEC_ERR_UNSUPPORTED, "sample %d has %d tree nodes", b, T);
+    const int S = seq_lens[b];
+    if (S < 0) return fail(SPEC_ERR_INVALID, "seq_lens[%d] = %d", b, S);
+    if ((int64_t)S + T > kv->cap[sample_ids[b]])
+      return fail(SPEC_ERR_CAPACITY, "sample %d: %d committed + %d nodes exceed capacity %d", b, S,
+                  T, kv->cap[sample_ids[b]]);
+    const int t0 = tree_offsets[b];
+    if (tree_parents[t0] != -1) return fail(SPEC_ERR_TREE, "sample %d: root parent must be -1", b);
+    for (int i = 0; i < T; ++i) {
+      const int tok = tree_tokens[t0 + i];
+      if (tok < 0 || tok >= cfg->vocab)
+        return fail(SPEC_ERR_TREE, "sample %d node %d: token %d out of range", b, i, tok);
+      if (i > 0) {
+        const int p = tree_parents[t0 + i];
+        if (p < 0 || p >= i)
+          return fail(SPEC_ERR_TREE, "sample %d node %d: parent %d not before the node", b, i, p);
+      }
+    }
+  }
+  const int N = tree_offsets[batch];
+  const size_t need = ws_layout(cfg, batch, N).total;
+  if (ws_bytes < need) return fail(SPEC_ERR_WORKSPACE, "workspace %zu bytes, needs %zu", ws_bytes, need);
+
+  // ---- planning ----
+  const int L = cfg->n_layers, H = cfg->hidden, nq = cfg->n_heads, nkv = cfg->n_kv_heads;
+  const int hd = cfg->head_dim, G = nq / nkv, F = cfg->ffn, V = cfg->vocab;
+  const WsLayout ly = ws_layout(cfg, batch, N);
+  char* ws = (char*)workspace;
+  hipStream_t s = (hipStream_t)stream;
+
+  std::vector<SampleInfo> si(batch);
+  for (int b = 0; b < batch; ++b) {
+    const int id = sample_ids[b];
+    si[b] = SampleInfo{kv->base[id], kv->cap[id], seq_lens[b], tree_offsets[b],
+                       tree_offsets[b + 1] - tree_offsets[b], 0, 0};
+  }
+  // Split-KV plan: a row tile is 32 query rows of one (sample, kv head).
+  int64_t key_work = 0, row_tiles = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int64_t tiles = (int64_t)(si[b].ntok * G + 31) / 32;
+    row_tiles += tiles * nkv;
+    key_work += tiles * nkv * (si[b].seq_len + si[b].ntok);
+  }
+  int64_t chunk = std::max<int64_t>(kMinChunk, (key_work + kTargetItems - 1) / kTargetItems);
+  chunk = (chunk + 127) / 128 * 128;
+  auto slots_for = [&](int64_t c) {
+    int64_t slots = 0;
+    for (int b = 0; b < batch; ++b) {
+      const int64_t ns = (si[b].seq_len + si[b].ntok + c - 1) / c;
+      if (ns > 1) slots += ns * nkv * ((si[b].ntok * G + 31) / 32);
+    }
+    return slots;
+  };
+  while (slots_for(chunk) > kPartCap) chunk *= 2;
+  std::vector<AttnItem> items;
+  std::vector<CombineItem> comb;
+  items.reserve(row_tiles * 2);
+  int part = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int keys = si[b].seq_len + si[b].ntok;
+    const int ns = (int)((keys + chunk - 1) / chunk);
+    const int tiles = (si[b].ntok * G + 31) / 32;
+    for (int g = 0; g < nkv; ++g)
+      for (int t = 0; t < tiles; ++t) {
+        if (ns > 1) comb.push_back(CombineItem{b, g, t * 32, ns, part, 0, 0, 0});
+        for (int k = 0; k < ns; ++k) {
+          const int k0 = (int)(k * chunk), k1 = (int)std::min<int64_t>(keys, (k + 1) * chunk);
+          items.push_back(AttnItem{b, g, t * 32, k0, k1, ns, ns > 1 ? part + k : 0, 0});
+        }
+        if (ns > 1) part += ns;
+      }
+  }
+
+  // ---- one upload of the per-call descriptors ----
+  const size_t o_si = 0;
+  const size_t o_tok = align_up(batch * sizeof(SampleInfo));
+  const size_t o_par = o_tok + align_up((size_t)N * 4);
+  const size_t o_items = o_par + align_up((size_t)N * 4);
+  const size_t o_comb = o_items + align_up(items.size() * sizeof(AttnItem));
+  const size_t blob_bytes = o_comb + comb.size() * sizeof(CombineItem);
+  std::vector<char> blob(blob_bytes, 0);
+  memcpy(blob.data() + o_si, si.data(), batch * sizeof(SampleInfo));
+  memcpy(blob.data() + o_tok, tree_tokens, (size_t)N * 4);
+  memcpy(blob.data() + o_par, tree_parents, (size_t)N * 4);
+  memcpy(blob.data() + o_items, items.data(), items.size() * sizeof(AttnItem));
+  if (!comb.empty()) memcpy(blob.data() + o_comb, comb.data(), comb.size() * sizeof(CombineItem));
+  if (int rc = stage_upload(kv, blob.data(), blob_bytes, ws + ly.blob, s)) return rc;
+
+  const SampleInfo* d_si = (const SampleInfo*)(ws + ly.blob + o_si);
+  const int32_t* d_tok = (const int32_t*)(ws + ly.blob + o_tok);
+  const int32_t* d_par = (const int32_t*)(ws + ly.blob + o_par);
+  const AttnItem* d_items = (const AttnItem*)(ws + ly.blob + o_items);
+  const CombineItem* d_comb = (const CombineItem*)(ws + ly.blob + o_comb);
+  TokInfo* d_toks = (TokInfo*)(ws + ly.toks);
+  uint64_t* d_anc = (uint64_t*)(ws + ly.anc);
+  float2* d_rope = (float2*)(ws + ly.rope);
+  float* d_x = (float*)(ws + ly.x);
+  bf16* d_h = (bf16*)(ws + ly.h);
+  bf16* d_q = (bf16*)(ws + ly.q);
+  bf16* d_o = (bf16*)(ws + ly.o);
+  bf16* d_act = (bf16*)(ws + ly.act);
+  float* d_lmv = (float*)(ws + ly.lm_val);
+  int32_t* d_lmi = (int32_t*)(ws + ly.lm_idx);
+  int32_t* d_arg = (int32_t*)(ws + ly.argmax);
+
+  const spec_debug nodbg{};
+  const spec_debug& D = dbg ? *dbg : nodbg;
+
+  // ---- the step ----
+  HIP_TRY(launch_tree_meta(d_si, batch, d_par, d_toks, d_anc, D.depth, D.pos, D.anc, s), "tree meta");
+  HIP_TRY(launch_rope_table(d_toks, N, hd, cfg->rope_theta, d_rope, s), "rope table");
+  HIP_TRY(launch_embed(d_tok, (const bf16*)w->tok_embed, d_x, N, H, s), "embed");
+
+  GemmArgs ga{};
+  ga.M = N;
+  ga.samples = d_si;
+  ga.toks = d_toks;
+  ga.kv_pool = kv->pool;
+  ga.n_kv_heads = nkv;
+  ga.head_dim = hd;
+  ga.rope_cs = d_rope;
+  AttnArgs aa{};
+  aa.q = d_q;
+  aa.kv_pool = kv->pool;
+  aa.samples = d_si;
+  aa.toks = d_toks;
+  aa.anc = d_anc;
+  aa.items = d_items;
+  aa.n_items = (int)items.size();
+  aa.part_o = (float*)(ws + ly.part_o);
+  aa.part_ml = (float*)(ws + ly.part_ml);
+  aa.out = d_o;
+  aa.n_heads = nq;
+  aa.n_kv_heads = nkv;
+  aa.head_dim = hd;
+  aa.comb = d_comb;
+  aa.n_comb = (int)comb.size();
+
+  for (int l = 0; l < L; ++l) {
+    HIP_TRY(launch_rmsnorm(d_x, (const bf16*)w->attn_norm[l], d_h, N, H, cfg->rms_eps, s), "rmsnorm");
+    GemmArgs g = ga;
+    g.A = d_h;
+    g.K = H;
+    g.B0 = (const bf16*)w->wq[l];
+    g.B1 = (const bf16*)w->wk[l];
+    g.B2 = (const bf16*)w->wv[l];
+    g.n0 = nq * hd;
+    g.n1 = g.n2 = nkv * hd;
+    g.N = g.n0 + g.n1 + g.n2;
+    g.q_out = d_q;
+    g.layer = l;
+    HIP_TRY(timed(SPEC_K_GEMM_QKV, s, [&] { return launch_gemm(EPI_QKV, g, s); }), "qkv gemm");
+    aa.layer = l;
+    HIP_TRY(timed(SPEC_K_ATTENTION, s, [&] { return launch_attention(aa, s); }), "attention");
+    g = ga;
+    g.A = d_o;
+    g.K = nq * hd;
+    g.B0 = (const bf16*)w->wo[l];
+    g.n0 = g.N = H;
+    g.x = d_x;
+    HIP_TRY(timed(SPEC_K_GEMM_O, s, [&] { return launch_gemm(EPI_RESID, g, s); }), "o gemm");
+    HIP_TRY(launch_rmsnorm(d_x, (const bf16*)w->ffn_norm[l], d_h, N, H, cfg->rms_eps, s), "rmsnorm");
+    g = ga;
+    g.A = d_h;
+    g.K = H;
+    g.B0 = (const bf16*)w->w_gate[l];
+    g.B1 = (const bf16*)w->w_up[l];
+    g.n0 = g.n1 = F;
+    g.N = 2 * F;
+    g.act_out = d_act;
+    HIP_TRY(timed(SPEC_K_GEMM_GATE_UP, s, [&] { return launch_gemm(EPI_GATE_UP, g, s); }), "gate/up gemm");
+    g = ga;
+    g.A = d_act;
+    g.K = F;
+    g.B0 = (const bf16*)w->w_down[l];
+    g.n0 = g.N = H;
+    g.x = d_x;
+    HIP_TRY(timed(SPEC_K_GEMM_DOWN, s, [&] { return launch_gemm(EPI_RESID, g, s); }), "down gemm");
+  }
+  HIP_TRY(launch_rmsnorm(d_x, (const bf16*)w->final_norm, d_h, N, H, cfg->rms_eps, s), "rmsnorm");
+  {
+    GemmArgs g = ga;
+    g.A = d_h;
+    g.K = H;
+    g.B0 = (const bf16*)w->lm_head;
+    g.n0 = g.N = V;
+    g.part_val = d_lmv;
+    g.part_idx = d_lmi;
+    g.logits = D.logits;
+    HIP_TRY(timed(SPEC_K_LM_HEAD, s, [&] { return launch_gemm(EPI_ARGMAX, g, s); }), "lm head");
+  }
+  HIP_TRY(launch_argmax_reduce(d_lmv, d_lmi, N, V / 64, d_arg, D.argmax, s), "argmax");
+  HIP_TRY(launch_accept(d_si, batch, d_tok, d_par, d_toks, d_arg, accepted_len, next_token,
+                        accepted_nodes, s),
+          "accept");
+  return SPEC_OK;
+}
+
+SPEC_API int spec_kv_commit(spec_kv* kv, int32_t batch, const int32_t* sample_ids,
+                            const int32_t* seq_lens, const int32_t* accepted_len,
+                            const int32_t* accepted_nodes, int32_t* new_seq_lens, void* stream) {
+  g_err.clear();
+  if (!kv || !sample_ids || !seq_lens || !accepted_len || !accepted_nodes || !new_seq_lens)
+    return fail(SPEC_ERR_INVALID, "null argument");
+  if (batch < 1 || batch > kv->n) return fail(SPEC_ERR_INVALID, "batch %d out of range", batch);
+  if (int rc = check_samples(kv, batch, sample_ids)) return rc;
+  std::vector<SampleInfo> si(batch);
+  for (int b = 0; b < batch; ++b) {
+    const int id = sample_ids[b];
+    if (seq_lens[b] < 0 || seq_lens[b] >= kv->cap[id])
+      return fail(SPEC_ERR_CAPACITY, "seq_lens[%d] = %d outside capacity %d", b, seq_lens[b], kv->cap[id]);
+    si[b] = SampleInfo{kv->base[id], kv->cap[id], seq_lens[b], 0, SPEC_MAX_TREE, 0, 0};
+  }
+  hipStream_t s = (hipStream_t)stream;
+  void* ctl = (char*)kv->pool + kv->ctl_off;
+  if (int rc = stage_upload(kv, si.data(), batch * sizeof(SampleInfo), ctl, s)) return rc;
+  const spec_model_config& c = kv->cfg;
+  HIP_TRY(timed(SPEC_K_COMMIT, s, [&] {
+            return launch_compact((const SampleInfo*)ctl, batch, kv->pool, c.n_layers,
+                                  c.n_kv_heads, c.head_dim, accepted_len, accepted_nodes,
+                                  new_seq_lens, s);
+          }),
+          "compact");
+  return SPEC_OK;
+}
+
+SPEC_API int spec_profile_begin(int32_t kernel_class, int32_t max_launches) {
+  if (kernel_class < 0 || kernel_class >= SPEC_K_COUNT || max_launches < 1)
+    return fail(SPEC_ERR_INVALID, "bad profile request");
+  for (auto e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof.ev.assign(2 * (size_t)max_launches, nullptr);
+  for (auto& e : g_prof.ev) HIP_TRY(hipEventCreate(&e), "profile event");
+  g_prof.kind = kernel_class;
+  g_prof.max = max_launches;
+  g_prof.count = 0;
+  g_prof.on = true;
+  return SPEC_OK;
+}
+
+SPEC_API int spec_profile_end(float* total_ms, int32_t* launches) {
+  if (!total_ms || !launches) return fail(SPEC_ERR_INVALID, "null argument");
+  g_prof.on = false;
+  float tot = 0.f;
+  for (int i = 0; i < g_prof.count; ++i) {
+    HIP_TRY(hipEventSynchronize(g_prof.ev[2 * i + 1]), "profile sync");
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]), "profile elapsed");
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = g_prof.count;
+  for (auto e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof.ev.clear();
+  g_prof.count = 0;
+  return SPEC_OK;
+}

@@ -1,0 +1,124 @@
+// Shared device types, descriptors and launcher prototypes of the
+// specverify library (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spec {
+
+typedef __bf16 bf16;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+typedef __attribute__((ext_vector_type(2))) int i32x2;
+
+constexpr int kMaxTree = 64;
+constexpr int kWave = 64;
+
+// Per live sample, built on the host for every verify call.
+struct SampleInfo {
+  int64_t kv_base;   // element offset of the sample's block in the KV pool
+  int32_t cap;       // positions per (layer, K/V, kv head)
+  int32_t seq_len;   // committed length S_b
+  int32_t tok0;      // first node row of the sample in the batch
+  int32_t ntok;      // T_b
+  int32_t pad0, pad1;
+};
+static_assert(sizeof(SampleInfo) == 32, "SampleInfo layout");
+
+// Per node row, written by the metadata kernel.
+struct TokInfo {
+  int32_t sample;    // live-sample index b
+  int32_t node;      // node index inside its tree
+  int32_t pos;       // rotary position S_b + depth
+  int32_t depth;
+};
+static_assert(sizeof(TokInfo) == 16, "TokInfo layout");
+
+// One attention work item: a tile of up to 32 query rows of one
+// (sample, kv head) against the key range [key0, key1) of its cache.
+// Query row r of a (sample, kv head) is (node r / G, query head kvh*G + r % G).
+struct AttnItem {
+  int32_t sample, kvh, row0, key0, key1, nsplit, part, pad;
+};
+static_assert(sizeof(AttnItem) == 32, "AttnItem layout");
+
+// One split-combine job: nsplit partial tiles starting at slot part0.
+struct CombineItem {
+  int32_t sample, kvh, row0, nsplit, part0, pad0, pad1, pad2;
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (each returns hipGetLastError() of its launch)
+// ---------------------------------------------------------------------------
+
+enum GemmEpilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_GATE_UP = 2, EPI_ARGMAX = 3 };
+
+struct GemmArgs {
+  const bf16* A;          // [M][K] activations
+  int M, K;
+  // Weight segments (row-major [rows][K]); virtual columns run through them
+  // in order.
+  const bf16* B0; const bf16* B1; const bf16* B2;
+  int n0, n1, n2;         // rows of each segment
+  int N;                  // n0 + n1 + n2 (EPI_GATE_UP: 2 * ffn)
+  // EPI_QKV
+  bf16* q_out;            // [M][n_heads*head_dim]
+  bf16* kv_pool;
+  const SampleInfo* samples;
+  const TokInfo* toks;
+  int layer, n_kv_heads, head_dim;
+  const float2* rope_cs;  // [M][head_dim/2] (cos, sin) of each row's angles
+  // EPI_RESID
+  float* x;               // [M][N] residual, x += A.B^T
+  // EPI_GATE_UP
+  bf16* act_out;          // [M][ffn]
+  // EPI_ARGMAX
+  float* part_val;        // [M][N/64]
+  int32_t* part_idx;
+  float* logits;          // optional [M][N]
+};
+
+hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
+
+struct AttnArgs {
+  const bf16* q;            // [N][n_heads*head_dim]
+  const bf16* kv_pool;
+  const SampleInfo* samples;
+  const TokInfo* toks;
+  const uint64_t* anc;      // [N]
+  const AttnItem* items;
+  int n_items;
+  float* part_o;            // [slots][32][head_dim]
+  float* part_ml;           // [slots][32][2]
+  bf16* out;                // [N][n_heads*head_dim]
+  int layer, n_heads, n_kv_heads, head_dim;
+  const CombineItem* comb;
+  int n_comb;
+};
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+hipError_t launch_tree_meta(const SampleInfo* samples, int batch, const int32_t* parents,
+                            TokInfo* toks, uint64_t* anc, int32_t* dbg_depth, int32_t* dbg_pos,
+                            uint64_t* dbg_anc, hipStream_t s);
+hipError_t launch_rope_table(const TokInfo* toks, int n, int head_dim, float theta, float2* cs,
+                             hipStream_t s);
+hipError_t launch_embed(const int32_t* tokens, const bf16* table, float* x, int n, int hidden,
+                        hipStream_t s);
+hipError_t launch_rmsnorm(const float* x, const bf16* gain, bf16* out, int n, int hidden,
+                          float eps, hipStream_t s);
+hipError_t launch_argmax_reduce(const float* part_val, const int32_t* part_idx, int n, int parts,
+                                int32_t* argmax, int32_t* dbg_argmax, hipStream_t s);
+hipError_t launch_accept(const SampleInfo* samples, int batch, const int32_t* tokens,
+                         const int32_t* parents, const TokInfo* toks, const int32_t* argmax,
+                         int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
+                         hipStream_t s);
+hipError_t launch_compact(const SampleInfo* samples, int batch, bf16* kv_pool, int n_layers,
+                          int n_kv_heads, int head_dim, const int32_t* accepted_len,
+                          const int32_t* accepted_nodes, int32_t* new_seq_lens, hipStream_t s);
+
+}  // namespace spec

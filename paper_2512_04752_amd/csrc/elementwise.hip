@@ -1,0 +1,255 @@
+// The small kernels of the verify step: tree metadata, rotary angle table,
+// embedding gather, RMSNorm, the final argmax reduction, greedy tree
+// acceptance and KV compaction.
+#include <math.h>
+
+#include "common.h"
+
+namespace spec {
+
+namespace {
+
+// Depth, position and ancestor set of every node: one thread per sample
+// walks its tree in node order (parents come first).
+__global__ void tree_meta_kernel(const SampleInfo* samples, int batch, const int32_t* parents,
+                                 TokInfo* toks, uint64_t* anc, int32_t* dbg_depth,
+                                 int32_t* dbg_pos, uint64_t* dbg_anc) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= batch) return;
+  const SampleInfo s = samples[b];
+  for (int i = 0; i < s.ntok; ++i) {
+    const int row = s.tok0 + i;
+    int depth = 0;
+    uint64_t set = 1ull;
+    if (i > 0) {
+      const int p = parents[row];
+      depth = toks[s.tok0 + p].depth + 1;
+      set = anc[s.tok0 + p] | (1ull << i);
+    }
+    toks[row] = TokInfo{b, i, s.seq_len + depth, depth};
+    anc[row] = set;
+    if (dbg_depth) dbg_depth[row] = depth;
+    if (dbg_pos) dbg_pos[row] = s.seq_len + depth;
+    if (dbg_anc) dbg_anc[row] = set;
+  }
+}
+
+// cos/sin of position * theta^(-2j/d), angles in double precision.
+__global__ void rope_table_kernel(const TokInfo* toks, int n, int half, int head_dim, double theta,
+                                  float2* cs) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n * half) return;
+  const int row = idx / half, j = idx % half;
+  const double freq = pow(theta, -2.0 * (double)j / (double)head_dim);
+  const double ang = (double)toks[row].pos * freq;
+  double sn, cn;
+  sincos(ang, &sn, &cn);
+  cs[idx] = make_float2((float)cn, (float)sn);
+}
+
+__global__ void embed_kernel(const int32_t* tokens, const bf16* table, float* x, int hidden) {
+  const int row = blockIdx.x;
+  const bf16* src = table + (size_t)tokens[row] * hidden;
+  float* dst = x + (size_t)row * hidden;
+  for (int c = threadIdx.x * 8; c < hidden; c += blockDim.x * 8) {
+    const bf16x8 v = *(const bf16x8*)(src + c);
+    f32x4 lo = {(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+    f32x4 hi = {(float)v[4], (float)v[5], (float)v[6], (float)v[7]};
+    *(f32x4*)(dst + c) = lo;
+    *(f32x4*)(dst + c + 4) = hi;
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+  return v;
+}
+
+// out = bf16(x / sqrt(mean(x^2) + eps) * gain), one 256-thread block per row.
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* x, const bf16* gain, bf16* out,
+                                                      int hidden, float eps) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const float* xr = x + (size_t)row * hidden;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < hidden; c += 256 * 4) {
+    const f32x4 v = *(const f32x4*)(xr + c);
+    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float rstd = rsqrtf(tot / (float)hidden + eps);
+  bf16* orow = out + (size_t)row * hidden;
+  for (int c = threadIdx.x * 4; c < hidden; c += 256 * 4) {
+    const f32x4 v = *(const f32x4*)(xr + c);
+    const bf16x4 g = *(const bf16x4*)(gain + c);
+    bf16x4 y;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) y[k] = (bf16)(v[k] * rstd * (float)g[k]);
+    *(bf16x4*)(orow + c) = y;
+  }
+}
+
+// Row maximum over the LM-head partials; ties go to the lowest token id.
+__global__ __launch_bounds__(64) void argmax_reduce_kernel(const float* part_val,
+                                                           const int32_t* part_idx, int parts,
+                                                           int32_t* argmax, int32_t* dbg_argmax) {
+  const int row = blockIdx.x;
+  float v = -INFINITY;
+  int idx = 0x7fffffff;
+  for (int p = threadIdx.x; p < parts; p += 64) {
+    const float pv = part_val[(size_t)row * parts + p];
+    const int pi = part_idx[(size_t)row * parts + p];
+    if (pv > v || (pv == v && pi < idx)) { v = pv; idx = pi; }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(v, m);
+    const int oi = __shfl_xor(idx, m);
+    if (ov > v || (ov == v && oi < idx)) { v = ov; idx = oi; }
+  }
+  if (threadIdx.x == 0) {
+    if (idx == 0x7fffffff) idx = 0;   // every logit NaN: report token 0
+    argmax[row] = idx;
+    if (dbg_argmax) dbg_argmax[row] = idx;
+  }
+}
+
+// Greedy tree acceptance, one thread per sample: a node is accepted when its
+// parent is and its token is the parent's greedy successor; the deepest
+// accepted node (lowest index on ties) ends the accepted branch.
+__global__ void accept_kernel(const SampleInfo* samples, int batch, const int32_t* tokens,
+                              const int32_t* parents, const TokInfo* toks, const int32_t* argmax,
+                              int32_t* accepted_len, int32_t* next_token,
+                              int32_t* accepted_nodes) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= batch) return;
+  const SampleInfo s = samples[b];
+  uint64_t acc = 1ull;
+  int best = 0, best_depth = 0;
+  for (int i = 1; i < s.ntok; ++i) {
+    const int row = s.tok0 + i;
+    const int p = parents[row];
+    if (((acc >> p) & 1ull) && tokens[row] == argmax[s.tok0 + p]) {
+      acc |= 1ull << i;
+      const int d = toks[row].depth;
+      if (d > best_depth) { best_depth = d; best = i; }
+    }
+  }
+  accepted_len[b] = best_depth;
+  next_token[b] = argmax[s.tok0 + best];
+  int32_t* out = accepted_nodes + (size_t)b * kMaxTree;
+  for (int d = best_depth + 1; d < kMaxTree; ++d) out[d] = -1;
+  int node = best;
+  for (int d = best_depth; d >= 0; --d) {
+    out[d] = node;
+    node = (node > 0) ? parents[s.tok0 + node] : 0;
+  }
+}
+
+// Move the accepted branch of one (sample, layer, K/V head) to positions
+// S_b + 1 .. S_b + accepted_len.  Sources (S_b + node, node >= depth) can be
+// destinations of shallower entries, so every source row is read into
+// registers before any row is written.
+template <int HD>
+__global__ __launch_bounds__(256) void compact_kernel(const SampleInfo* samples, bf16* kv_pool,
+                                                      int n_kv_heads, const int32_t* accepted_len,
+                                                      const int32_t* accepted_nodes,
+                                                      int32_t* new_seq_lens) {
+  constexpr int DC = HD / 8;
+  constexpr int PER = (kMaxTree * DC + 255) / 256;
+  const int b = blockIdx.x, layer = blockIdx.y, kvh2 = blockIdx.z;
+  const SampleInfo s = samples[b];
+  int acc = accepted_len[b];
+  if (acc < 0) acc = 0;
+  if (acc > s.ntok - 1) acc = s.ntok - 1;
+  if (s.seq_len + acc >= s.cap) acc = s.cap - 1 - s.seq_len;
+  if (layer == 0 && kvh2 == 0 && threadIdx.x == 0) new_seq_lens[b] = s.seq_len + acc + 1;
+  if (acc == 0) return;
+  bf16* base = kv_pool + s.kv_base + ((size_t)layer * 2 * n_kv_heads + kvh2) * s.cap * HD;
+  const int32_t* nodes = accepted_nodes + (size_t)b * kMaxTree;
+  i32x4 v[PER];
+  int dst[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int q = threadIdx.x + 256 * k;
+    const int d = 1 + q / DC, c = q % DC;
+    dst[k] = -1;
+    if (d <= acc) {
+      const int nd = nodes[d];
+      if (nd > d && nd < s.ntok && s.seq_len + nd < s.cap) {
+        v[k] = *(const i32x4*)(base + (size_t)(s.seq_len + nd) * HD + c * 8);
+        dst[k] = (s.seq_len + d) * HD + c * 8;
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < PER; ++k)
+    if (dst[k] >= 0) *(i32x4*)(base + dst[k]) = v[k];
+}
+
+}  // namespace
+
+hipError_t launch_tree_meta(const SampleInfo* samples, int batch, const int32_t* parents,
+                            TokInfo* toks, uint64_t* anc, int32_t* dbg_depth, int32_t* dbg_pos,
+                            uint64_t* dbg_anc, hipStream_t s) {
+  tree_meta_kernel<<<(batch + 63) / 64, 64, 0, s>>>(samples, batch, parents, toks, anc, dbg_depth,
+                                                     dbg_pos, dbg_anc);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(const TokInfo* toks, int n, int head_dim, float theta, float2* cs,
+                             hipStream_t s) {
+  const int half = head_dim / 2;
+  const int total = n * half;
+  rope_table_kernel<<<(total + 255) / 256, 256, 0, s>>>(toks, n, half, head_dim, (double)theta, cs);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed(const int32_t* tokens, const bf16* table, float* x, int n, int hidden,
+                        hipStream_t s) {
+  embed_kernel<<<n, 256, 0, s>>>(tokens, table, x, hidden);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const float* x, const bf16* gain, bf16* out, int n, int hidden,
+                          float eps, hipStream_t s) {
+  rmsnorm_kernel<<<n, 256, 0, s>>>(x, gain, out, hidden, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_reduce(const float* part_val, const int32_t* part_idx, int n, int parts,
+                                int32_t* argmax, int32_t* dbg_argmax, hipStream_t s) {
+  argmax_reduce_kernel<<<n, 64, 0, s>>>(part_val, part_idx, parts, argmax, dbg_argmax);
+  return hipGetLastError();
+}
+
+hipError_t launch_accept(const SampleInfo* samples, int batch, const int32_t* tokens,
+                         const int32_t* parents, const TokInfo* toks, const int32_t* argmax,
+                         int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
+                         hipStream_t s) {
+  accept_kernel<<<(batch + 63) / 64, 64, 0, s>>>(samples, batch, tokens, parents, toks, argmax,
+                                                 accepted_len, next_token, accepted_nodes);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const SampleInfo* samples, int batch, bf16* kv_pool, int n_layers,
+                          int n_kv_heads, int head_dim, const int32_t* accepted_len,
+                          const int32_t* accepted_nodes, int32_t* new_seq_lens, hipStream_t s) {
+  const dim3 grid(batch, n_layers, 2 * n_kv_heads);
+  if (head_dim == 128)
+    compact_kernel<128><<<grid, 256, 0, s>>>(samples, kv_pool, n_kv_heads, accepted_len,
+                                             accepted_nodes, new_seq_lens);
+  else if (head_dim == 64)
+    compact_kernel<64><<<grid, 256, 0, s>>>(samples, kv_pool, n_kv_heads, accepted_len,
+                                            accepted_nodes, new_seq_lens);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace spec

@@ -1,0 +1,195 @@
+"""Shared pieces of the GPU parity tests: building a workload on the device,
+running the oracle on the same bits, and the comparison rules.
+
+Comparison rules (tolerance of the verify step on bf16 logits):
+* logits: |z_gpu - z_oracle| <= ATOL + RTOL * |z_oracle| element-wise;
+* greedy tokens: equal, or "tie-excused" where the oracle's logit of the
+  GPU's choice is within ATOL of the oracle's maximum;
+* acceptance: bit-exact against the oracle's acceptance run on the GPU's own
+  greedy tokens, and end to end equal to the oracle wherever the two agree
+  on every greedy token of the sample;
+* depth, positions, ancestor sets, compacted KV positions: bit-exact.
+"""
+
+import sys
+import time
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2512_04752_amd as sv
+import workload as wl
+
+ATOL, RTOL = 3e-2, 2e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def cpu_weights(W):
+    return {"tok_embed": W["tok_embed"].cpu(), "final_norm": W["final_norm"].cpu(),
+            "lm_head": W["lm_head"].cpu(),
+            "layers": [{k: v.cpu() for k, v in lw.items()} for lw in W["layers"]]}
+
+
+def prefix_for_oracle(ver, ids, lens):
+    ks, vs = [], []
+    for i, S in zip(ids, lens):
+        k, v = ver.kv.sample_view(int(i))
+        ks.append(k[:, :, :int(S)].cpu())
+        vs.append(v[:, :, :int(S)].cpu())
+    return ks, vs
+
+
+def run_gpu(ver, ids, trees, lens, logits=True):
+    """One verify through the C ABI with debug dumps; returns host results."""
+    n = sum(len(t[0]) for t in trees)
+    dbg = ver.debug_buffers(n, logits=logits)
+    acc, nxt, nodes = ver.verify(ids, trees, lens, debug=dbg)
+    torch.cuda.synchronize()
+    out = {k: v.cpu() for k, v in dbg.items()}
+    out["accepted_len"] = acc.cpu().tolist()
+    out["next_token"] = nxt.cpu().tolist()
+    out["nodes"] = nodes.cpu()
+    return out
+
+
+def split_rows(trees):
+    offs = [0]
+    for t in trees:
+        offs.append(offs[-1] + len(t[0]))
+    return offs
+
+
+def check_logits(z_gpu, z_or, what=""):
+    z_or = z_or.to(torch.float64)
+    z_gpu = z_gpu.to(torch.float64)
+    err = (z_gpu - z_or).abs()
+    bound = ATOL + RTOL * z_or.abs()
+    bad = (err > bound)
+    rel = (err / z_or.abs().clamp_min(1e-3)).max().item()
+    say(f"  logits {what}: max_abs {err.max().item():.3e} max_rel {rel:.3e} "
+        f"violations {int(bad.sum())}/{bad.numel()}")
+    assert not bad.any(), f"{what}: {int(bad.sum())} logits outside tolerance, max err {err.max()}"
+
+
+def check_argmax(g_gpu, z_or):
+    """Returns the number of tie-excused disagreements; fails on others."""
+    g_or = torch.argmax(z_or, dim=-1)
+    excused = 0
+    for i in range(len(g_gpu)):
+        if int(g_gpu[i]) != int(g_or[i]):
+            row = z_or[i]
+            assert row[int(g_gpu[i])] >= row.max() - ATOL, \
+                f"node {i}: gpu {int(g_gpu[i])} vs oracle {int(g_or[i])}, margin " \
+                f"{(row.max() - row[int(g_gpu[i])]).item():.4f}"
+            excused += 1
+    return excused
+
+
+def check_sample_acceptance(tokens, parents, g_gpu_b, gpu_len, gpu_next, gpu_nodes,
+                            or_res=None, b=None, g_or_b=None):
+    """Bit-exact: the oracle's acceptance on the GPU's greedy tokens equals the
+    GPU's; and equal to the oracle's own result when all greedy tokens agree."""
+    a, nx, path = oracle.greedy_accept(tokens, parents, g_gpu_b)
+    assert (gpu_len, gpu_next) == (a, nx)
+    nodes = gpu_nodes.tolist()
+    assert nodes[:a + 1] == path and all(x == -1 for x in nodes[a + 1:])
+    if or_res is not None and list(g_gpu_b) == list(g_or_b):
+        assert or_res["accepted_len"][b] == a and or_res["path"][b] == path
+        assert or_res["next_token"][b] == nx
+
+
+def check_meta(trees, lens, out):
+    offs = split_rows(trees)
+    for b, (tokens, parents) in enumerate(trees):
+        depth, anc = oracle.tree_metadata(parents)
+        sl = slice(offs[b], offs[b + 1])
+        assert out["depth"][sl].tolist() == depth.tolist()
+        assert out["pos"][sl].tolist() == (int(lens[b]) + depth).tolist()
+        bits = [sum(1 << j for j in range(len(parents)) if anc[i, j]) for i in range(len(parents))]
+        got = [int(x) & ((1 << 64) - 1) for x in out["anc"][sl].tolist()]
+        assert got == bits
+
+
+def full_check(cfg, W_cpu, ver, ids, trees, lens, check_ids=None):
+    """GPU verify of the whole batch; oracle on samples ``check_ids`` (all by
+    default).  Returns (gpu result, oracle result, excused count)."""
+    t0 = time.time()
+    out = run_gpu(ver, ids, trees, lens)
+    say(f"  gpu verify done ({time.time() - t0:.1f}s)")
+    check_meta(trees, lens, out)
+    offs = split_rows(trees)
+    g_gpu = out["argmax"].tolist()
+    # acceptance on the GPU's own greedy tokens: every sample, bit-exact
+    for b, (tokens, parents) in enumerate(trees):
+        check_sample_acceptance(tokens, parents, g_gpu[offs[b]:offs[b + 1]],
+                                out["accepted_len"][b], out["next_token"][b], out["nodes"][b])
+    if check_ids is None:
+        check_ids = list(range(len(trees)))
+    pk, pv = prefix_for_oracle(ver, [ids[b] for b in check_ids], [lens[b] for b in check_ids])
+    t0 = time.time()
+    r = oracle.verify(cfg, W_cpu, pk, pv, [lens[b] for b in check_ids],
+                      [trees[b] for b in check_ids])
+    say(f"  oracle on {len(check_ids)} samples done ({time.time() - t0:.1f}s)")
+    rows = torch.cat([torch.arange(offs[b], offs[b + 1]) for b in check_ids])
+    check_logits(out["logits"][rows], r["logits"], f"{len(rows)} rows")
+    excused = check_argmax(out["argmax"][rows], r["logits"])
+    roffs = split_rows([trees[b] for b in check_ids])
+    g_or = r["argmax"].tolist()
+    for j, b in enumerate(check_ids):
+        tokens, parents = trees[b]
+        check_sample_acceptance(tokens, parents, g_gpu[offs[b]:offs[b + 1]],
+                                out["accepted_len"][b], out["next_token"][b], out["nodes"][b],
+                                r, j, g_or[roffs[j]:roffs[j + 1]])
+    say(f"  tie-excused argmax disagreements: {excused}")
+    return out, r, excused
+
+
+def check_tree_kv(cfg, ver, ids, trees, lens, r, check_ids):
+    """K/V the verify wrote at slots S_b + node equal the oracle's (tolerance)."""
+    for j, b in enumerate(check_ids):
+        k, v = ver.kv.sample_view(int(ids[b]))
+        S, T = int(lens[b]), len(trees[b][0])
+        kg = k[:, :, S:S + T].cpu().to(torch.float64)
+        vg = v[:, :, S:S + T].cpu().to(torch.float64)
+        for got, want, name in ((kg, r["tree_k"][j], "K"), (vg, r["tree_v"][j], "V")):
+            err = (got - want).abs()
+            assert (err <= ATOL + RTOL * want.abs()).all(), f"tree {name} max err {err.max()}"
+
+
+def tiny_setup(seed=0, batch=4, chain=4, extra_cap=64):
+    """The 2-layer workload: bf16-rounded weights, oracle prefill of each
+    128-token prompt written into the pool, root = the oracle's greedy token
+    after the prompt, chain drafts following the oracle's greedy choice."""
+    cfg = wl.TINY
+    w = wl.tiny_workload(seed, batch=batch, chain=chain)
+    W_cpu = wl.make_weights(cfg, 10 + seed, device="cpu", dtype=torch.bfloat16)
+    W_dev = {"tok_embed": W_cpu["tok_embed"].cuda(), "final_norm": W_cpu["final_norm"].cuda(),
+             "lm_head": W_cpu["lm_head"].cuda(),
+             "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
+    caps = [int(s) + extra_cap for s in w.seq_lens]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=batch, max_tokens=batch * 64)
+    for b, prompt in enumerate(w.prompts):
+        pk, pv, logits = oracle.prefill(cfg, W_cpu, prompt, cache_dtype=torch.bfloat16)
+        k, v = ver.kv.sample_view(b)
+        k[:, :, :len(prompt)].copy_(pk.cuda())
+        v[:, :, :len(prompt)].copy_(pv.cuda())
+        w.trees[b][0][0] = int(torch.argmax(logits[-1]))
+    torch.cuda.synchronize()
+    return cfg, w, W_cpu, W_dev, ver
+
+
+def oracle_greedy_fn(cfg, W_cpu, ver, ids, lens):
+    pk, pv = prefix_for_oracle(ver, ids, lens)
+
+    def fn(trees):
+        r = oracle.verify(cfg, W_cpu, pk, pv, lens, trees)
+        offs = split_rows(trees)
+        g = r["argmax"].tolist()
+        return [g[offs[b]:offs[b + 1]] for b in range(len(trees))]
+
+    return fn

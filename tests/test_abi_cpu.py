@@ -1,0 +1,198 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, exports
+every entry point the header declares, sizes KV pools and workspaces, carves
+pools, and rejects malformed calls before touching the device."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2512_04752_amd as sv
+import workload as wl
+from paper_2512_04752_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specverify.h")
+
+# A plausible device address for pure host-side calls; never dereferenced,
+# since every call below fails validation or touches no device memory.
+FAKE_DEV = 0x7F0000000000
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\*?\s+\**(spec_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    L = sv.lib()
+    declared = header_functions()
+    assert declared, "no declarations parsed"
+    assert sorted(B.EXPORTS) == declared
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_kv_bytes_arithmetic():
+    cfg = wl.TINY
+    caps = [100, 37, 1]
+    per = lambda cap: (cfg.n_layers * 2 * cfg.n_kv_heads * cap * cfg.head_dim * 2 + 255) // 256 * 256
+    ctl = (len(caps) * 32 + 255) // 256 * 256
+    assert sv.spec_kv_bytes(cfg, caps) == sum(per(c) for c in caps) + ctl
+    assert sv.spec_kv_bytes(cfg, [0]) == 0
+    bad = wl.ModelConfig(2, 256, 4, 2, 32, 1024, 1024)          # head_dim 32 unsupported
+    assert sv.spec_kv_bytes(bad, [10]) == 0
+
+
+def test_kv_alloc_carves_contiguous_blocks():
+    cfg = wl.LLAMA_8B
+    caps = [1000, 17, 2048]
+    need = sv.spec_kv_bytes(cfg, caps)
+    L = sv.lib()
+    c = B.make_config(cfg)
+    arr = (ctypes.c_int32 * 3)(*caps)
+    h = ctypes.c_void_p()
+    assert L.spec_kv_alloc(ctypes.byref(c), 3, arr, ctypes.c_void_p(FAKE_DEV), need - 1,
+                           ctypes.byref(h)) == -3
+    assert L.spec_kv_alloc(ctypes.byref(c), 3, arr, ctypes.c_void_p(FAKE_DEV + 8), need,
+                           ctypes.byref(h)) == -1          # misaligned
+    assert L.spec_kv_alloc(ctypes.byref(c), 3, arr, ctypes.c_void_p(FAKE_DEV), need,
+                           ctypes.byref(h)) == 0
+    offs = [sv.spec_kv_sample_layout(h, i) for i in range(3)]
+    assert offs[0] == (0, 1000)
+    blk = lambda cap: cfg.n_layers * 2 * cfg.n_kv_heads * cap * cfg.head_dim * 2
+    assert offs[1] == (blk(1000), 17)
+    assert offs[2][0] == offs[1][0] + (blk(17) + 255) // 256 * 256
+    with pytest.raises(sv.SpecError):
+        sv.spec_kv_sample_layout(h, 3)
+    sv.spec_kv_free(h)
+
+
+def test_workspace_bytes_monotone():
+    cfg = wl.LLAMA_8B
+    a = sv.spec_workspace_bytes(cfg, 4, 256)
+    b = sv.spec_workspace_bytes(cfg, 128, 1024)
+    c = sv.spec_workspace_bytes(cfg, 256, 16384)
+    assert 0 < a < b < c
+    assert sv.spec_workspace_bytes(cfg, 0, 10) == 0
+    assert sv.spec_workspace_bytes(cfg, 10, 5) == 0
+    # the 16384-token sweep cell fits comfortably in one GPU's HBM
+    assert c < 8 << 30
+
+
+class FakeVerify:
+    """spec_verify with fake device pointers: only for calls that must fail
+    validation (the library checks everything before any device work)."""
+
+    def __init__(self, cfg=wl.TINY, caps=(200, 200, 200)):
+        self.cfg = cfg
+        self.c = B.make_config(cfg)
+        self.L = sv.lib()
+        arr = (ctypes.c_int32 * len(caps))(*caps)
+        need = sv.spec_kv_bytes(cfg, list(caps))
+        self.kv = ctypes.c_void_p()
+        assert self.L.spec_kv_alloc(ctypes.byref(self.c), len(caps), arr,
+                                    ctypes.c_void_p(FAKE_DEV), need, ctypes.byref(self.kv)) == 0
+        n = cfg.n_layers
+        self.ptrs = {k: (ctypes.c_void_p * n)(*[FAKE_DEV] * n) for k in B.Weights.LAYER_FIELDS}
+        self.w = B.spec_weights(FAKE_DEV, FAKE_DEV, FAKE_DEV,
+                                *[ctypes.cast(self.ptrs[k], ctypes.POINTER(ctypes.c_void_p))
+                                  for k in B.Weights.LAYER_FIELDS])
+
+    def call(self, ids, trees, lens, ws_bytes=None):
+        offs, toks, pars = sv.flatten_trees(trees)
+        if ws_bytes is None:
+            ws_bytes = sv.spec_workspace_bytes(self.cfg, len(ids), int(offs[-1]))
+        i = lambda a: B._i32(a)
+        (a1, p1), (a2, p2), (a3, p3), (a4, p4), (a5, p5) = (i(ids), i(offs), i(toks), i(pars),
+                                                            i(lens))
+        rc = self.L.spec_verify(ctypes.byref(self.c), ctypes.byref(self.w), self.kv, len(ids), p1,
+                                p2, p3, p4, p5, ctypes.c_void_p(FAKE_DEV), ws_bytes, None,
+                                ctypes.c_void_p(FAKE_DEV), ctypes.c_void_p(FAKE_DEV),
+                                ctypes.c_void_p(FAKE_DEV), None)
+        return rc, self.L.spec_last_error().decode()
+
+    def close(self):
+        self.L.spec_kv_free(self.kv)
+
+
+@pytest.fixture
+def fake():
+    f = FakeVerify()
+    yield f
+    f.close()
+
+
+GOOD = ([5, 6, 7], [-1, 0, 0])
+
+
+@pytest.mark.parametrize("case,code", [
+    ("root_parent", -2), ("parent_after", -2), ("parent_self", -2), ("token_range", -2),
+    ("negative_token", -2), ("empty_tree", -2), ("too_big_tree", -6), ("capacity", -3),
+    ("dup_sample", -1), ("bad_sample", -1), ("workspace", -5), ("neg_len", -1),
+])
+def test_validation_errors(fake, case, code):
+    ids, trees, lens, ws = [0, 1], [GOOD, GOOD], [10, 10], None
+    if case == "root_parent":
+        trees = [GOOD, ([1, 2], [0, 0])]
+    elif case == "parent_after":
+        trees = [GOOD, ([1, 2, 3], [-1, 2, 0])]
+    elif case == "parent_self":
+        trees = [GOOD, ([1, 2, 3], [-1, 0, 2])]
+    elif case == "token_range":
+        trees = [GOOD, ([1, 1024], [-1, 0])]
+    elif case == "negative_token":
+        trees = [GOOD, ([1, -3], [-1, 0])]
+    elif case == "empty_tree":
+        trees = [GOOD, ([], [])]
+    elif case == "too_big_tree":
+        trees = [GOOD, ([1] * 65, wl.chain_tree(65))]
+    elif case == "capacity":
+        lens = [10, 198]
+    elif case == "dup_sample":
+        ids = [1, 1]
+    elif case == "bad_sample":
+        ids = [0, 3]
+    elif case == "workspace":
+        ws = 1000
+    elif case == "neg_len":
+        lens = [10, -1]
+    rc, msg = fake.call(ids, trees, lens, ws)
+    assert rc == code, msg
+    assert msg
+
+
+def test_unsupported_shape_rejected():
+    L = sv.lib()
+    bad = B.make_config(wl.ModelConfig(2, 200, 4, 2, 64, 1024, 1024))   # hidden % 128 != 0
+    arr = (ctypes.c_int32 * 1)(10)
+    h = ctypes.c_void_p()
+    assert L.spec_kv_alloc(ctypes.byref(bad), 1, arr, ctypes.c_void_p(FAKE_DEV), 1 << 30,
+                           ctypes.byref(h)) == -6
+    assert b"hidden" in L.spec_last_error()
+
+
+def test_commit_validation(fake):
+    L = fake.L
+    ids = (ctypes.c_int32 * 2)(0, 0)
+    lens = (ctypes.c_int32 * 2)(5, 5)
+    assert L.spec_kv_commit(fake.kv, 2, ids, lens, ctypes.c_void_p(FAKE_DEV),
+                            ctypes.c_void_p(FAKE_DEV), ctypes.c_void_p(FAKE_DEV), None) == -1
+    ids = (ctypes.c_int32 * 1)(0)
+    lens = (ctypes.c_int32 * 1)(200)
+    assert L.spec_kv_commit(fake.kv, 1, ids, lens, ctypes.c_void_p(FAKE_DEV),
+                            ctypes.c_void_p(FAKE_DEV), ctypes.c_void_p(FAKE_DEV), None) == -3
+
+
+def test_flatten_trees():
+    offs, toks, pars = sv.flatten_trees([([1, 2], [-1, 0]), ([3], [-1])])
+    assert offs.tolist() == [0, 2, 3] and toks.tolist() == [1, 2, 3] and pars.tolist() == [-1, 0, -1]
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        B.lib()

@@ -1,0 +1,251 @@
+"""GPU parity of the verify step against the oracle, through the C ABI.
+
+Small workloads are compared element by element on every output; the full
+1B / 8B workloads run whole on the GPU (in the launch configuration the
+benchmark times) and are compared on seeded subsets of samples, which is
+exact because samples never interact in a verify step.
+"""
+
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_04752_amd as sv
+import workload as wl
+from tests.gpu_util import (ATOL, check_argmax, check_logits, check_sample_acceptance,
+                            check_tree_kv, cpu_weights, full_check, oracle_greedy_fn,
+                            prefix_for_oracle, run_gpu, say, split_rows, tiny_setup)
+
+pytestmark = pytest.mark.gpu
+
+
+def pool_bytes(ver, sample, lo, hi):
+    k, v = ver.kv.sample_view(sample)
+    return k[:, :, lo:hi].clone(), v[:, :, lo:hi].clone()
+
+
+# ---------------------------------------------------------------------------
+# the 2-layer workload
+# ---------------------------------------------------------------------------
+
+def test_tiny_workload_parity():
+    say("tiny workload: 4 samples, prompt 128, chain 4")
+    cfg, w, W_cpu, W_dev, ver = tiny_setup(0)
+    ids, lens = list(range(4)), w.seq_lens.tolist()
+    rng = np.random.default_rng(0)
+    wl.follow_greedy(w.trees, w.branches, w.p_follow, oracle_greedy_fn(cfg, W_cpu, ver, ids, lens),
+                     rng)
+    before = [pool_bytes(ver, b, 0, lens[b]) for b in ids]
+    out, r, exc = full_check(cfg, W_cpu, ver, ids, w.trees, lens)
+    check_tree_kv(cfg, ver, ids, w.trees, lens, r, list(range(4)))
+    for b in ids:   # the committed prefix is never written
+        k, v = pool_bytes(ver, b, 0, lens[b])
+        assert torch.equal(k, before[b][0]) and torch.equal(v, before[b][1])
+    assert sum(out["accepted_len"]) > 0
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_tiny_random_trees_and_commit(seed):
+    """Random-numbered trees whose deepest branch follows greedy: accepted
+    branches with node ids != depth, so committing moves K/V."""
+    say(f"tiny random trees seed {seed}")
+    cfg, w, W_cpu, W_dev, ver = tiny_setup(seed, extra_cap=64)
+    rng = np.random.default_rng(seed)
+    ids, lens = list(range(4)), w.seq_lens.tolist()
+    trees, branches = [], []
+    for b in ids:
+        par = wl.recursive_tree(rng, 24, 6, 3)
+        toks = wl.random_tokens(rng, 24, cfg.vocab)
+        toks[0] = w.trees[b][0][0]
+        trees.append((toks, par))
+        branches.append(wl.deepest_branch(par, rng))
+    wl.follow_greedy(trees, branches, 1.0, oracle_greedy_fn(cfg, W_cpu, ver, ids, lens), rng)
+    out, r, exc = full_check(cfg, W_cpu, ver, ids, trees, lens)
+    check_tree_kv(cfg, ver, ids, trees, lens, r, ids)
+    # commit: positions S+d take the K/V of accepted node path[d], bitwise
+    pre = [pool_bytes(ver, b, 0, lens[b] + 24) for b in ids]
+    new_lens = ver.commit(ids, lens)
+    torch.cuda.synchronize()
+    new_lens = new_lens.cpu().tolist()
+    moved = 0
+    for b in ids:
+        acc = out["accepted_len"][b]
+        path = out["nodes"][b][:acc + 1].tolist()
+        assert new_lens[b] == lens[b] + acc + 1
+        k, v = pool_bytes(ver, b, 0, lens[b] + acc + 1)
+        S = lens[b]
+        assert torch.equal(k[:, :, :S], pre[b][0][:, :, :S])
+        assert torch.equal(v[:, :, :S], pre[b][1][:, :, :S])
+        for d, node in enumerate(path):
+            assert torch.equal(k[:, :, S + d], pre[b][0][:, :, S + node])
+            assert torch.equal(v[:, :, S + d], pre[b][1][:, :, S + node])
+            moved += int(node != d)
+    say(f"  accepted {out['accepted_len']}, rows moved {moved}")
+    assert moved > 0
+
+
+def test_tiny_edge_cases():
+    """Permuted subset of the pool, empty prefix, one-node trees, a 64-node
+    tree, a star with duplicate sibling tokens, ragged sizes."""
+    cfg = wl.TINY
+    say("tiny edge cases")
+    W_cpu = wl.make_weights(cfg, 33, dtype=torch.bfloat16)
+    W_dev = {"tok_embed": W_cpu["tok_embed"].cuda(), "final_norm": W_cpu["final_norm"].cuda(),
+             "lm_head": W_cpu["lm_head"].cuda(),
+             "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
+    caps = [300, 90, 70, 400, 64, 200]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=6, max_tokens=6 * 64)
+    rng = np.random.default_rng(4)
+    gen = torch.Generator(device="cuda").manual_seed(4)
+    ids = [4, 0, 2, 5, 1]
+    lens = [0, 236, 5, 130, 26]
+    for i, S in zip(ids, lens):
+        k, v = ver.kv.sample_view(i)
+        wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+    star_tok = wl.random_tokens(rng, 1, cfg.vocab) + [7, 7, 9, 7, 9]
+    trees = [
+        (wl.random_tokens(rng, 64, cfg.vocab), wl.recursive_tree(rng, 64, 8, 4)),
+        (wl.random_tokens(rng, 1, cfg.vocab), [-1]),
+        (star_tok, [-1, 0, 0, 0, 0, 0]),
+        (wl.random_tokens(rng, 33, cfg.vocab), wl.chain_tree(33)),
+        (wl.random_tokens(rng, 37, cfg.vocab), wl.recursive_tree(rng, 37, 5, 4)),
+    ]
+    # the 64-node sample has an empty prefix: cap 64 holds exactly its tree
+    full_check(cfg, W_cpu, ver, ids, trees, lens)
+
+
+def test_tiny_repeat_is_bitwise_identical():
+    say("tiny repeatability")
+    cfg, w, W_cpu, W_dev, ver = tiny_setup(5)
+    ids, lens = list(range(4)), w.seq_lens.tolist()
+    a = run_gpu(ver, ids, w.trees, lens)
+    ka = [pool_bytes(ver, b, 0, lens[b] + 4) for b in ids]
+    b_ = run_gpu(ver, ids, w.trees, lens)
+    kb = [pool_bytes(ver, b, 0, lens[b] + 4) for b in ids]
+    assert torch.equal(a["logits"], b_["logits"])
+    assert torch.equal(a["argmax"], b_["argmax"])
+    assert a["accepted_len"] == b_["accepted_len"] and torch.equal(a["nodes"], b_["nodes"])
+    for x, y in zip(ka, kb):
+        assert torch.equal(x[0], y[0]) and torch.equal(x[1], y[1])
+
+
+def test_tiny_multistep_matches_greedy_decoding():
+    """Verify + commit rounds with chain drafts (the oracle's greedy stream,
+    each draft token replaced at random with p = 0.3) reproduce the oracle's
+    plain greedy decoding token for token, up to a tie-excused divergence."""
+    say("tiny multi-step")
+    cfg, w, W_cpu, W_dev, ver = tiny_setup(6, batch=1, extra_cap=64)
+    S0 = int(w.seq_lens[0])
+    pk, pv = prefix_for_oracle(ver, [0], [S0])
+    root = w.trees[0][0][0]
+    # the oracle's own greedy decoding (one-node trees), with its logits
+    ks, vs, lens = pk, pv, [S0]
+    want, zs, cur = [root], [], root
+    for _ in range(28):
+        r = oracle.verify(cfg, W_cpu, ks, vs, lens, [([cur], [-1])])
+        zs.append(r["logits"][0])
+        cur = r["next_token"][0]
+        want.append(cur)
+        ks, vs, lens = oracle.commit(ks, vs, lens, r)
+    rng = np.random.default_rng(6)
+    got, S, steps = [root], S0, 0
+    while len(got) < 24:
+        n0 = len(got)
+        draft = [got[-1]] + [want[n0 + j] if rng.random() > 0.3 else int(rng.integers(cfg.vocab))
+                             for j in range(3)]
+        acc, nxt, nodes = ver.verify([0], [(draft, wl.chain_tree(4))], [S])
+        new_len = ver.commit([0], [S])
+        torch.cuda.synchronize()
+        a, n = int(acc[0]), int(nxt[0])
+        assert nodes[0, :a + 1].tolist() == list(range(a + 1))
+        emitted = draft[1:a + 1] + [n]
+        for t in emitted:
+            j = len(got)
+            if t != want[j]:
+                z = zs[j - 1]
+                assert z[t] >= z.max() - ATOL, f"stream diverges at {j} without a tie"
+                say(f"  tie-excused divergence at token {j}")
+                return
+            got.append(t)
+        S += a + 1
+        assert int(new_len[0]) == S
+        steps += 1
+    say(f"  {len(got)} tokens in {steps} steps")
+    assert steps < 23
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads, checked on sample subsets
+# ---------------------------------------------------------------------------
+
+def device_setup(w, W_dev, cap_extra=0, seed=0):
+    cfg = w.cfg
+    caps = [int(s) + len(t[0]) + cap_extra for s, t in zip(w.seq_lens, w.trees)]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=w.batch, max_tokens=w.n_tokens)
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    for b, S in enumerate(w.seq_lens):
+        k, v = ver.kv.sample_view(b)
+        wl.fill_prefix_kv(k, v, int(S), wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    return ver
+
+
+def test_llama1b_workload_parity():
+    say("llama-1B shape: batch 32, KV U[512,2048], 15-node binary trees")
+    w = wl.llama1b_workload(1000)
+    W_dev = wl.make_weights(w.cfg, 1000, device="cuda")
+    W_cpu = cpu_weights(W_dev)
+    ver = device_setup(w, W_dev, seed=1)
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    check = [0, 11, 22, 31]
+    sub_trees = [w.trees[b] for b in check]
+    wl.follow_greedy(sub_trees, [w.branches[b] for b in check], w.p_follow,
+                     oracle_greedy_fn(w.cfg, W_cpu, ver, check, [lens[b] for b in check]),
+                     np.random.default_rng(1))
+    out, r, exc = full_check(w.cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check)
+    check_tree_kv(w.cfg, ver, ids, w.trees, lens, r, check)
+    del ver
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+@pytest.fixture(scope="module")
+def w8b():
+    say("generating 8B-shape weights on the GPU")
+    W_dev = wl.make_weights(wl.LLAMA_8B, 2000, device="cuda")
+    W_cpu = cpu_weights(W_dev)
+    yield W_dev, W_cpu
+    del W_dev, W_cpu
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def test_llama8b_early_phase_sampled(w8b):
+    say("llama-8B shape early phase: batch 128, lognormal KV, 8-node trees")
+    W_dev, W_cpu = w8b
+    w = wl.early_workload(2000)
+    ver = device_setup(w, W_dev, seed=2)
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    check = [int(np.argmax(w.seq_lens)), 77]
+    out, r, exc = full_check(w.cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check)
+    check_tree_kv(w.cfg, ver, ids, w.trees, lens, r, check)
+    del ver
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def test_llama8b_tail_phase_sampled(w8b):
+    say("llama-8B shape tail phase: batch 4, KV U[16384,32768], 64-node trees")
+    W_dev, W_cpu = w8b
+    w = wl.tail_workload(3000)
+    ver = device_setup(w, W_dev, seed=3)
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    check = [int(np.argmax(w.seq_lens))]
+    out, r, exc = full_check(w.cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check)
+    check_tree_kv(w.cfg, ver, ids, w.trees, lens, r, check)
+    del ver
+    gc.collect()
+    torch.cuda.empty_cache()
