@@ -1,0 +1,216 @@
+"""Benchmark of the batched tree-verify step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload early|tail|llama1b]
+
+A step is one verify (target forward over every draft tree, greedy
+acceptance) plus the commit (KV compaction) of the whole batch.  Inputs are
+synthetic with the shapes of the chosen workload, weights random with the
+model's architecture, all resident in HBM before timing starts.  Prints one
+JSON line: verified tokens/s as `value`, accepted tokens/s beside it, the
+roofline fraction of the dominant kernel (timed with HIP events on its own
+stream inside the timed region) and the oracle's throughput on the host cores
+over a bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tree-verify tokens/s & accepted tokens/s, Llama-3-8B shape, 1 MI355X"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="early", choices=["early", "tail", "llama1b"])
+    p.add_argument("--cpu-baseline", type=int, default=1, help="0 skips the oracle timing")
+    p.add_argument("--seed", type=int, default=None)
+    return p.parse_args()
+
+
+def describe(name, w):
+    if name == "early":
+        return ("Llama-3-8B-shape verify, early generation: batch 128, 8-node draft trees "
+                "(4 levels, width <= 3), KV lengths lognormal(median 1024, sigma 0.8) in [128, 8192]")
+    if name == "tail":
+        return ("Llama-3-8B-shape verify, long tail: batch 4, 64-node draft trees (8 levels, "
+                "<= 4 children), KV lengths U[16384, 32768]")
+    return ("Llama-3.2-1B-shape verify: batch 32, 15-node binary trees, KV lengths U[512, 2048]")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+
+    import paper_2512_04752_amd as sv
+    import workload as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    make = {"early": wl.early_workload, "tail": wl.tail_workload, "llama1b": wl.llama1b_workload}
+    w = make[args.workload]() if args.seed is None else make[args.workload](args.seed)
+    cfg = w.cfg
+    plain_trees = [(list(t[0]), list(t[1])) for t in w.trees]   # before greedy steering
+
+    t_setup = time.time()
+    W = wl.make_weights(cfg, w.seed, device="cuda")
+    caps = [int(s) + len(t[0]) for s, t in zip(w.seq_lens, w.trees)]
+    ver = sv.Verifier(cfg, W, caps, max_batch=w.batch, max_tokens=w.n_tokens)
+    gen = torch.Generator(device="cuda").manual_seed(w.seed)
+    for b, S in enumerate(w.seq_lens):
+        k, v = ver.kv.sample_view(b)
+        wl.fill_prefix_kv(k, v, int(S), wl.prefix_kv_std(cfg), gen)
+    ids = list(range(w.batch))
+    lens = [int(s) for s in w.seq_lens]
+
+    # Draft trees whose designated branch follows the target's greedy choice
+    # (p = 0.7 per level), built with untimed verify calls.
+    def greedy_fn(trees):
+        n = sum(len(t[0]) for t in trees)
+        dbg = ver.debug_buffers(n, logits=False)
+        ver.verify(ids, trees, lens, debug=dbg)
+        g = dbg["argmax"].cpu().tolist()
+        out, off = [], 0
+        for t in trees:
+            out.append(g[off:off + len(t[0])])
+            off += len(t[0])
+        return out
+
+    wl.follow_greedy(w.trees, w.branches, w.p_follow, greedy_fn, np.random.default_rng(w.seed))
+    flat = sv.flatten_trees(w.trees)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t_setup
+
+    stream = torch.cuda.current_stream()
+
+    def step():
+        ver.verify(ids, None, lens, flat=flat, stream=stream)
+        ver.commit(ids, lens, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    dominant = {"early": "gemm_gate_up", "llama1b": "gemm_gate_up", "tail": "attention"}[args.workload]
+    sv.spec_profile_begin(dominant, args.steps * cfg.n_layers + 8)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dom_ms, dom_launches = sv.spec_profile_end()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    acc = ver.accepted_len[:w.batch].cpu()
+    accepted = int(acc.sum().item()) + w.batch          # + the bonus token per sample
+    n_tok = w.n_tokens
+    value = n_tok / (ms_per_step / 1e3)
+    acc_rate = accepted / (ms_per_step / 1e3)
+
+    # Per-kernel-class time of one step, measured in separate untimed steps.
+    breakdown = {}
+    for kc in sv.binding.KERNEL_CLASS:
+        sv.spec_profile_begin(kc, 4 * cfg.n_layers + 8)
+        step()
+        torch.cuda.synchronize()
+        ms, n = sv.spec_profile_end()
+        breakdown[kc] = round(ms, 4)
+
+    # Roofline of the dominant kernel: algorithmic work of one launch.
+    H, F, d = cfg.hidden, cfg.ffn, cfg.head_dim
+    avg_ms = dom_ms / max(dom_launches, 1)
+    if dominant == "gemm_gate_up":
+        work = 2.0 * n_tok * (2 * F) * H                 # flops
+        achieved = work / (avg_ms / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": "gemm_bf16_kernel<EPI_GATE_UP>",
+                "work_per_launch": f"2*{n_tok}*{2 * F}*{H} flop"}
+    else:
+        kv_bytes = sum((int(S) + len(t[0])) for S, t in zip(w.seq_lens, w.trees)) * \
+            cfg.n_kv_heads * d * 2 * 2
+        qo_bytes = n_tok * cfg.n_heads * d * 2 * 2
+        work = kv_bytes + qo_bytes
+        achieved = work / (avg_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "kernel": "tree_attention_kernel<128> + attention_combine_kernel<128>",
+                "work_per_launch": f"{work} bytes (K/V of every key once, q in, o out)"}
+    roof["avg_launch_ms"] = round(avg_ms, 5)
+    roof["launches"] = dom_launches
+
+    # Composite roofline of the whole step.
+    gemm_flops = 2.0 * n_tok * cfg.gemm_params()
+    attn_bytes = sum((int(S) + len(t[0])) for S, t in zip(w.seq_lens, w.trees)) * \
+        cfg.kv_bytes_per_token()
+    weight_bytes = 2.0 * cfg.gemm_params()
+    t_roof = max(gemm_flops / (PEAK_BF16_TFLOPS * 1e12), weight_bytes / (PEAK_HBM_GBS * 1e9)) + \
+        attn_bytes / (PEAK_HBM_GBS * 1e9)
+
+    result = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (random weights of the named shape, synthetic KV and draft trees)",
+        "config": {"workload": describe(args.workload, w), "model": "llama-3-8b-shape"
+                   if cfg.hidden == 4096 else "llama-3.2-1b-shape",
+                   "batch": w.batch, "tokens_per_step": n_tok,
+                   "kv_tokens": int(sum(lens)), "parallelism": "none (1 GPU)"},
+        "accepted_tokens_per_s": round(acc_rate, 1),
+        "accepted_per_sample_per_step": round(accepted / w.batch, 3),
+        "roofline": roof,
+        "step_roofline": {"t_roof_ms": round(t_roof * 1e3, 4),
+                          "frac": round(t_roof * 1e3 / ms_per_step, 4)},
+        "breakdown_ms_per_step": breakdown,
+        "setup_s": round(setup_s, 1),
+    }
+
+    if args.cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok,
+                                              ms_per_step)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok, ms_per_step):
+    """The oracle, untuned, on the host cores over a bounded sample: the first
+    sample(s) of the same workload with their unsteered draft trees."""
+    import torch
+
+    import oracle
+
+    Wc = {"tok_embed": W["tok_embed"].cpu(), "final_norm": W["final_norm"].cpu(),
+          "lm_head": W["lm_head"].cpu(),
+          "layers": [{k: v.cpu() for k, v in lw.items()} for lw in W["layers"]]}
+    n_s = 1 if cfg.hidden == 4096 else 2
+    sel = list(range(n_s))
+    pk = [ver.kv.sample_view(b)[0][:, :, :lens[b]].cpu() for b in sel]
+    pv = [ver.kv.sample_view(b)[1][:, :, :lens[b]].cpu() for b in sel]
+    t0 = time.perf_counter()
+    oracle.verify(cfg, Wc, pk, pv, [lens[b] for b in sel], [plain_trees[b] for b in sel])
+    dt = time.perf_counter() - t0
+    toks = sum(len(plain_trees[b][0]) for b in sel)
+    return {"value": round(toks / dt, 4), "unit": "tokens/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"{n_s} sample(s) of the same workload ({toks} tree nodes, KV lengths "
+                      f"{[lens[b] for b in sel]}), float64 torch-CPU oracle, {dt:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

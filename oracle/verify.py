@@ -37,6 +37,15 @@ previously verified KV cache untouched):
 
 Readings of points the paper leaves open are listed with the function
 that applies them.
+
+Precision.  By default every step is exact float64 arithmetic: the plain
+definition.  ``operand_dtype=torch.bfloat16`` instead rounds every operand
+of every matrix product to bfloat16 (RMSNorm outputs, q/k/v, the softmax
+numerators, the attention output, the SwiGLU activation; weights and cached
+K/V already are bfloat16) and keeps everything else exact.  That is an ideal
+bf16-operand computation of the same definition; the tests use it only to
+measure how far bf16 storage alone moves the logits of a deep random-weight
+model, which sets the tolerance for full-depth comparisons.
 """
 
 from __future__ import annotations
@@ -142,12 +151,18 @@ def rope(x: torch.Tensor, cos: torch.Tensor, sin: torch.Tensor) -> torch.Tensor:
     return torch.cat([a * c - b * s, b * c + a * s], dim=-1)
 
 
-def attention(q, k_all, v_all, visible, n_kv_heads):
+def _identity(t):
+    return t
+
+
+def attention(q, k_all, v_all, visible, n_kv_heads, rnd=_identity):
     """Masked softmax attention for one sample.
 
     q: [T, nq, d]; k_all, v_all: [nkv, S+T, d]; visible: bool [T, S+T].
     Query head ``h`` reads KV head ``h // (nq / nkv)`` (grouped-query
-    attention).  Scores are scaled by 1/sqrt(d).
+    attention).  Scores are scaled by 1/sqrt(d); the softmax is
+    exp(s - max s) / sum exp(s - max s), and ``rnd`` is applied to its
+    numerators where they enter the product with V.
     """
     T, nq, d = q.shape
     group = nq // n_kv_heads
@@ -156,12 +171,12 @@ def attention(q, k_all, v_all, visible, n_kv_heads):
         kv = h // group
         s = (q[:, h, :] @ k_all[kv].T) / math.sqrt(d)
         s = s.masked_fill(~visible, float("-inf"))
-        p = torch.softmax(s, dim=-1)
-        out[:, h, :] = p @ v_all[kv]
+        e = torch.exp(s - s.max(dim=-1, keepdim=True).values)
+        out[:, h, :] = (rnd(e) @ v_all[kv]) / e.sum(dim=-1, keepdim=True)
     return out
 
 
-def forward(cfg, W, samples):
+def forward(cfg, W, samples, operand_dtype=None):
     """Target-model forward over the nodes of several samples.
 
     ``samples`` is a list of dicts with keys ``tokens`` (list[int]),
@@ -170,8 +185,14 @@ def forward(cfg, W, samples):
     ([L, nkv, S, d]; S may be 0).  Every new token sees the whole prefix.
 
     Returns the float64 logits [sum T, V] and, per sample, the new tokens'
-    post-rotation keys and values [L, nkv, T, d].
+    post-rotation keys and values [L, nkv, T, d].  ``operand_dtype``: see the
+    module docstring.
     """
+    if operand_dtype is None:
+        rnd = _identity
+    else:
+        def rnd(t):
+            return t.to(operand_dtype).to(F64)
     L, nq, nkv, d = cfg.n_layers, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
     tokens = [t for s in samples for t in s["tokens"]]
     starts = []
@@ -189,12 +210,12 @@ def forward(cfg, W, samples):
 
     for l in range(L):
         lw = W["layers"][l]
-        h = rms_norm(x, _f64(lw["attn_norm"]), cfg.rms_eps)
+        h = rnd(rms_norm(x, _f64(lw["attn_norm"]), cfg.rms_eps))
         q = (h @ _f64(lw["wq"]).T).view(N, nq, d)
         k = (h @ _f64(lw["wk"]).T).view(N, nkv, d)
-        v = (h @ _f64(lw["wv"]).T).view(N, nkv, d)
-        q = rope(q, cos, sin)
-        k = rope(k, cos, sin)
+        v = rnd((h @ _f64(lw["wv"]).T).view(N, nkv, d))
+        q = rnd(rope(q, cos, sin))
+        k = rnd(rope(k, cos, sin))
         o = torch.zeros(N, nq, d, dtype=F64)
         for b, s in enumerate(samples):
             lo, T = starts[b], len(s["tokens"])
@@ -208,14 +229,14 @@ def forward(cfg, W, samples):
             k_all = torch.cat([pk, kb], dim=1)
             v_all = torch.cat([pv, vb], dim=1)
             visible = torch.cat([torch.ones(T, S, dtype=torch.bool), s["visible_tree"]], dim=1)
-            o[lo:lo + T] = attention(q[lo:lo + T], k_all, v_all, visible, nkv)
-        x = x + o.reshape(N, nq * d) @ _f64(lw["wo"]).T
-        h2 = rms_norm(x, _f64(lw["ffn_norm"]), cfg.rms_eps)
+            o[lo:lo + T] = attention(q[lo:lo + T], k_all, v_all, visible, nkv, rnd)
+        x = x + rnd(o.reshape(N, nq * d)) @ _f64(lw["wo"]).T
+        h2 = rnd(rms_norm(x, _f64(lw["ffn_norm"]), cfg.rms_eps))
         gate = h2 @ _f64(lw["w_gate"]).T
         up = h2 @ _f64(lw["w_up"]).T
-        x = x + (torch.nn.functional.silu(gate) * up) @ _f64(lw["w_down"]).T
+        x = x + rnd(torch.nn.functional.silu(gate) * up) @ _f64(lw["w_down"]).T
 
-    hf = rms_norm(x, _f64(W["final_norm"]), cfg.rms_eps)
+    hf = rnd(rms_norm(x, _f64(W["final_norm"]), cfg.rms_eps))
     logits = hf @ _f64(W["lm_head"]).T
     return logits, new_k, new_v
 
@@ -224,7 +245,7 @@ def forward(cfg, W, samples):
 # The verify step, its commit, and a prefill built from the same forward
 # ---------------------------------------------------------------------------
 
-def verify(cfg, W, prefix_k, prefix_v, seq_lens, trees):
+def verify(cfg, W, prefix_k, prefix_v, seq_lens, trees, operand_dtype=None):
     """One batched tree-verify step.
 
     prefix_k[b], prefix_v[b]: committed K/V of sample b, [L, nkv, >= S_b, d]
@@ -254,7 +275,7 @@ def verify(cfg, W, prefix_k, prefix_v, seq_lens, trees):
             raise ValueError("prefix K/V shorter than seq_len")
         samples.append({"tokens": [int(t) for t in tokens], "pos": S + depth,
                         "visible_tree": anc, "prefix_k": pk, "prefix_v": pv})
-    logits, new_k, new_v = forward(cfg, W, samples)
+    logits, new_k, new_v = forward(cfg, W, samples, operand_dtype)
     g = torch.argmax(logits, dim=-1)   # first maximal index = lowest id on ties
 
     acc_len, nxt, paths = [], [], []

@@ -2,9 +2,18 @@
 running the oracle on the same bits, and the comparison rules.
 
 Comparison rules (tolerance of the verify step on bf16 logits):
-* logits: |z_gpu - z_oracle| <= ATOL + RTOL * |z_oracle| element-wise;
+* shallow models (2 layers): |z_gpu - z_oracle| <= ATOL + RTOL * |z_oracle|
+  element-wise against the exact oracle;
+* full-depth models: bf16 storage noise alone moves deep random-weight
+  logits further than that (an ideal bf16-operand computation of the oracle
+  misses it too), so the GPU's error against the exact oracle must stay
+  inside the envelope of that ideal bf16 computation's error: mean, 99.9th
+  percentile and per-node relative L2 error at most ENV_FACTOR times the
+  ideal's (plus a small floor);
 * greedy tokens: equal, or "tie-excused" where the oracle's logit of the
-  GPU's choice is within ATOL of the oracle's maximum;
+  GPU's choice is within the comparison's tolerance of the oracle's maximum
+  (ATOL for shallow models; twice the GPU's largest logit error at depth,
+  the most by which two logits can swap order);
 * acceptance: bit-exact against the oracle's acceptance run on the GPU's own
   greedy tokens, and end to end equal to the oracle wherever the two agree
   on every greedy token of the sample;
@@ -22,6 +31,7 @@ import paper_2512_04752_amd as sv
 import workload as wl
 
 ATOL, RTOL = 3e-2, 2e-2
+ENV_FACTOR = 1.5
 
 
 def say(*a):
@@ -76,14 +86,37 @@ def check_logits(z_gpu, z_or, what=""):
     assert not bad.any(), f"{what}: {int(bad.sum())} logits outside tolerance, max err {err.max()}"
 
 
-def check_argmax(g_gpu, z_or):
+def check_envelope(z_gpu, z_or, z_ideal, what=""):
+    """Full-depth rule: the GPU's deviation from the exact oracle is no larger
+    than an ideal bf16-operand computation's, within ENV_FACTOR.  Returns the
+    tie tolerance (twice the GPU's largest error)."""
+    z_or = z_or.to(torch.float64)
+    e_gpu = (z_gpu.to(torch.float64) - z_or).abs()
+    e_ref = (z_ideal.to(torch.float64) - z_or).abs()
+    rr = lambda e: (e.norm(dim=-1) / z_or.norm(dim=-1)).max().item()
+    q = lambda e: torch.quantile(e.flatten()[:: max(1, e.numel() // 4_000_000)].float(), 0.999).item()
+    stats = {"mean": (e_gpu.mean().item(), e_ref.mean().item()),
+             "q999": (q(e_gpu), q(e_ref)), "rowrel": (rr(e_gpu), rr(e_ref)),
+             "max": (e_gpu.max().item(), e_ref.max().item())}
+    strict = (e_gpu > ATOL + RTOL * z_or.abs()).float().mean().item()
+    say(f"  logits {what} (gpu, ideal bf16): " +
+        " ".join(f"{k} {a:.3e}/{b:.3e}" for k, (a, b) in stats.items()) +
+        f"; strict-rule violations {strict:.4%}")
+    floor = {"mean": 1e-3, "q999": 5e-3, "rowrel": 1e-3}
+    for k, f in floor.items():
+        a, b = stats[k]
+        assert a <= ENV_FACTOR * b + f, f"{what}: {k} error {a:.4e} exceeds envelope {b:.4e}"
+    return 2 * stats["max"][0]
+
+
+def check_argmax(g_gpu, z_or, tol=ATOL):
     """Returns the number of tie-excused disagreements; fails on others."""
     g_or = torch.argmax(z_or, dim=-1)
     excused = 0
     for i in range(len(g_gpu)):
         if int(g_gpu[i]) != int(g_or[i]):
             row = z_or[i]
-            assert row[int(g_gpu[i])] >= row.max() - ATOL, \
+            assert row[int(g_gpu[i])] >= row.max() - tol, \
                 f"node {i}: gpu {int(g_gpu[i])} vs oracle {int(g_or[i])}, margin " \
                 f"{(row.max() - row[int(g_gpu[i])]).item():.4f}"
             excused += 1
@@ -115,9 +148,10 @@ def check_meta(trees, lens, out):
         assert got == bits
 
 
-def full_check(cfg, W_cpu, ver, ids, trees, lens, check_ids=None):
+def full_check(cfg, W_cpu, ver, ids, trees, lens, check_ids=None, envelope=False):
     """GPU verify of the whole batch; oracle on samples ``check_ids`` (all by
-    default).  Returns (gpu result, oracle result, excused count)."""
+    default).  ``envelope`` selects the full-depth rule.  Returns (gpu
+    result, oracle result, excused count)."""
     t0 = time.time()
     out = run_gpu(ver, ids, trees, lens)
     say(f"  gpu verify done ({time.time() - t0:.1f}s)")
@@ -136,8 +170,16 @@ def full_check(cfg, W_cpu, ver, ids, trees, lens, check_ids=None):
                       [trees[b] for b in check_ids])
     say(f"  oracle on {len(check_ids)} samples done ({time.time() - t0:.1f}s)")
     rows = torch.cat([torch.arange(offs[b], offs[b + 1]) for b in check_ids])
-    check_logits(out["logits"][rows], r["logits"], f"{len(rows)} rows")
-    excused = check_argmax(out["argmax"][rows], r["logits"])
+    if envelope:
+        t0 = time.time()
+        ri = oracle.verify(cfg, W_cpu, pk, pv, [lens[b] for b in check_ids],
+                           [trees[b] for b in check_ids], operand_dtype=torch.bfloat16)
+        say(f"  ideal bf16-operand oracle done ({time.time() - t0:.1f}s)")
+        tol = check_envelope(out["logits"][rows], r["logits"], ri["logits"], f"{len(rows)} rows")
+    else:
+        check_logits(out["logits"][rows], r["logits"], f"{len(rows)} rows")
+        tol = ATOL
+    excused = check_argmax(out["argmax"][rows], r["logits"], tol)
     roffs = split_rows([trees[b] for b in check_ids])
     g_or = r["argmax"].tolist()
     for j, b in enumerate(check_ids):
@@ -149,14 +191,17 @@ def full_check(cfg, W_cpu, ver, ids, trees, lens, check_ids=None):
     return out, r, excused
 
 
-def check_tree_kv(cfg, ver, ids, trees, lens, r, check_ids):
-    """K/V the verify wrote at slots S_b + node equal the oracle's (tolerance)."""
+def check_tree_kv(cfg, ver, ids, trees, lens, r, check_ids, layers=None):
+    """K/V the verify wrote at slots S_b + node equal the oracle's (strict
+    tolerance; ``layers`` limits the check, e.g. to the first layer of a
+    deep model, whose K/V carry no accumulated bf16 noise)."""
     for j, b in enumerate(check_ids):
         k, v = ver.kv.sample_view(int(ids[b]))
         S, T = int(lens[b]), len(trees[b][0])
-        kg = k[:, :, S:S + T].cpu().to(torch.float64)
-        vg = v[:, :, S:S + T].cpu().to(torch.float64)
-        for got, want, name in ((kg, r["tree_k"][j], "K"), (vg, r["tree_v"][j], "V")):
+        sl = slice(None) if layers is None else slice(0, layers)
+        kg = k[sl, :, S:S + T].cpu().to(torch.float64)
+        vg = v[sl, :, S:S + T].cpu().to(torch.float64)
+        for got, want, name in ((kg, r["tree_k"][j][sl], "K"), (vg, r["tree_v"][j][sl], "V")):
             err = (got - want).abs()
             assert (err <= ATOL + RTOL * want.abs()).all(), f"tree {name} max err {err.max()}"
 

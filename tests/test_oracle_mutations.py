@@ -23,8 +23,10 @@ MUTATIONS = {
     "siblings visible": ("anc[i] = anc[p]\n", "anc[i] = anc[p] | anc[i - 1]\n"),
     "score scale dropped": ("@ k_all[kv].T) / math.sqrt(d)", "@ k_all[kv].T)"),
     "gate and up swapped": ("silu(gate) * up)", "silu(up) * gate)"),
-    "ffn residual dropped": ("x = x + (torch.nn.functional.silu(gate) * up) @",
-                             "x = (torch.nn.functional.silu(gate) * up) @"),
+    "ffn residual dropped": ("x = x + rnd(torch.nn.functional.silu(gate) * up) @",
+                             "x = rnd(torch.nn.functional.silu(gate) * up) @"),
+    "softmax not normalised": ("/ e.sum(dim=-1, keepdim=True)", ""),
+    "mask not applied": ('s = s.masked_fill(~visible, float("-inf"))', "s = s"),
     "deepest-node tie toward higher index": ("depth[i] > depth[best]", "depth[i] >= depth[best]"),
     "acceptance ignores the parent": ("accepted[i] = accepted[p] and", "accepted[i] ="),
 }
