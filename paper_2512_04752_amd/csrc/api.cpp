@@ -45,6 +45,7 @@ constexpr size_t kAlign = 256;
 constexpr int kPartCap = 8192;          // split-KV partial tiles per call
 constexpr int kTargetItems = 2048;      // attention work-groups aimed for
 constexpr int kMinChunk = 256;          // keys per split, lower bound
+constexpr int kMaxSplits = 64;          // key ranges per row tile (combine kernel's table)
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -347,7 +348,10 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     row_tiles += tiles * nkv;
     key_work += tiles * nkv * (si[b].seq_len + si[b].ntok);
   }
+  int64_t max_keys = 0;
+  for (int b = 0; b < batch; ++b) max_keys = std::max<int64_t>(max_keys, si[b].seq_len + si[b].ntok);
   int64_t chunk = std::max<int64_t>(kMinChunk, (key_work + kTargetItems - 1) / kTargetItems);
+  chunk = std::max<int64_t>(chunk, (max_keys + kMaxSplits - 1) / kMaxSplits);
   chunk = (chunk + 127) / 128 * 128;
   auto slots_for = [&](int64_t c) {
     int64_t slots = 0;

@@ -226,31 +226,45 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
   }
 }
 
-// Merge the partial states of a row tile's key ranges.
+// Merge the partial states of a row tile's key ranges: one block per query
+// row, one thread per head dimension; the per-split weights are computed once
+// into LDS and every split's partial output is an independent load.
 template <int HD>
-__global__ __launch_bounds__(NT) void attention_combine_kernel(AttnArgs a) {
+__global__ __launch_bounds__(HD) void attention_combine_kernel(AttnArgs a) {
+  constexpr int MAXS = 64;
+  __shared__ float wgt[MAXS];
+  __shared__ float inv_l;
   const CombineItem ci = a.comb[blockIdx.x];
+  const int row = blockIdx.y;
   const SampleInfo si = a.samples[ci.sample];
   const int G = a.n_heads / a.n_kv_heads;
-  const int nq_hd = a.n_heads * HD;
-  for (int idx = threadIdx.x; idx < 32 * HD; idx += NT) {
-    const int row = idx / HD, d = idx % HD;
-    const int gr = ci.row0 + row;
-    const int nd = gr / G, hq = ci.kvh * G + gr % G;
-    if (nd >= si.ntok) continue;
+  const int gr = ci.row0 + row;
+  const int nd = gr / G, hq = ci.kvh * G + gr % G;
+  if (nd >= si.ntok) return;
+  const int d = threadIdx.x;
+  if (d < 64) {
     float M = -INFINITY;
-    for (int sp = 0; sp < ci.nsplit; ++sp)
+    for (int sp = d; sp < ci.nsplit; sp += 64)
       M = fmaxf(M, a.part_ml[((size_t)(ci.part0 + sp) * 32 + row) * 2]);
-    float O = 0.f, L = 0.f;
-    for (int sp = 0; sp < ci.nsplit; ++sp) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) M = fmaxf(M, __shfl_xor(M, m));
+    float L = 0.f;
+    for (int sp = d; sp < ci.nsplit; sp += 64) {
       const size_t slot = (size_t)(ci.part0 + sp) * 32 + row;
       const float ms = a.part_ml[slot * 2];
       const float f = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
-      O += f * a.part_o[slot * HD + d];
+      if (sp < MAXS) wgt[sp] = f;
       L += f * a.part_ml[slot * 2 + 1];
     }
-    a.out[(size_t)(si.tok0 + nd) * nq_hd + hq * HD + d] = (bf16)(O / L);
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) L += __shfl_xor(L, m);
+    if (d == 0) inv_l = 1.f / L;
   }
+  __syncthreads();
+  float O = 0.f;
+  for (int sp = 0; sp < ci.nsplit; ++sp)
+    O += wgt[sp] * a.part_o[((size_t)(ci.part0 + sp) * 32 + row) * HD + d];
+  a.out[(size_t)(si.tok0 + nd) * a.n_heads * HD + hq * HD + d] = (bf16)(O * inv_l);
 }
 
 }  // namespace
@@ -259,10 +273,10 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.n_items == 0) return hipSuccess;
   if (a.head_dim == 128) {
     tree_attention_kernel<128><<<a.n_items, NT, 0, s>>>(a);
-    if (a.n_comb) attention_combine_kernel<128><<<a.n_comb, NT, 0, s>>>(a);
+    if (a.n_comb) attention_combine_kernel<128><<<dim3(a.n_comb, 32), 128, 0, s>>>(a);
   } else if (a.head_dim == 64) {
     tree_attention_kernel<64><<<a.n_items, NT, 0, s>>>(a);
-    if (a.n_comb) attention_combine_kernel<64><<<a.n_comb, NT, 0, s>>>(a);
+    if (a.n_comb) attention_combine_kernel<64><<<dim3(a.n_comb, 32), 64, 0, s>>>(a);
   } else {
     return hipErrorInvalidValue;
   }
