@@ -77,12 +77,15 @@ struct GemmArgs {
   // EPI_GATE_UP
   bf16* act_out;          // [M][ffn]
   // EPI_ARGMAX
-  float* part_val;        // [M][N/64]
+  float* part_val;        // [M][gemm_parts(N, M)]
   int32_t* part_idx;
   float* logits;          // optional [M][N]
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
+// Number of (max, index) partials per row the EPI_ARGMAX launch for an
+// [M x N] product writes.
+int gemm_parts(int N, int M);
 
 struct AttnArgs {
   const bf16* q;            // [N][n_heads*head_dim]

@@ -8,37 +8,49 @@
 //                residual stream
 //   EPI_GATE_UP  gate and up projections of the same features side by side,
 //                emitting silu(gate) * up in bf16
-//   EPI_ARGMAX   LM head: per row, the (max, lowest index) over each 64
-//                columns, optionally also the fp32 logits
+//   EPI_ARGMAX   LM head: per row, the (max, lowest index) over each wave's
+//                column slab, optionally also the fp32 logits
 //
-// Tiling: 128 x 128 output tile per 256-thread work-group (4 waves, 2 x 2,
-// 64 x 64 each), K step 64, two LDS buffers (64 KB) so that one barrier per
-// K step suffices; the next K slice is fetched into registers while the
-// current one feeds v_mfma_f32_32x32x16_bf16.  Both operands are K-major, so
-// every lane reads 16 contiguous bytes per MFMA operand.  LDS rows are 128 B
-// with the 16-byte chunk index XOR-swizzled by (row & 7).
-//
-// Work-groups are dispatched round-robin over the 8 XCDs; the tile order is
-// remapped so that the M tiles sharing one weight tile run on the same XCD
-// and hit its L2 instead of HBM.
+// Structure (one 256-thread work-group = 4 waves in a 2 x 2 grid, output tile
+// BM x BN, each wave BM/2 x BN/2 built from 32 x 32 v_mfma_f32_32x32x16_bf16
+// blocks; K step 64):
+//   * operand tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 (no
+//     register staging) into a two-stage ring; the next K step is in flight
+//     while the current one is multiplied, and one barrier per K step both
+//     publishes the new stage and frees the old one;
+//   * each wave-load writes 1 KB = 8 tile rows of 128 bytes; the 16-byte chunk
+//     index of row r is XOR-ed with (r >> 1) & 7, which makes the MFMA operand
+//     reads (16 consecutive rows, one chunk) hit all 64 LDS banks once;
+//   * fragments of the next 16-wide k-step are read from LDS into a second
+//     register set while the current set feeds the MFMAs.
+// Work-groups are dealt round-robin over the 8 XCDs; the tile order is
+// remapped so that the M tiles sharing one weight tile run on one XCD and hit
+// its L2 instead of HBM.
 #include "common.h"
 
 namespace spec {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
+constexpr int BK = 64, NT = 256;
 
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * 128 + ((chunk ^ (row & 7)) << 4);
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void load_lds16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
 }
 
-// Weight row feeding tile-local virtual column u of column tile tn.
-template <int EPI>
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
+// Virtual-column mapping.  Column u of an output tile belongs to wave
+// wn = u / TN, MFMA block nb = (u % TN) / 32, lane column c = u % 32.  For
+// EPI_QKV and EPI_GATE_UP, blocks (2p, 2p+1) of a wave form pair p: rotary
+// partners (dims j, j + d/2) or (gate, up) of the same feature.
+template <int EPI, int BN>
 __device__ __forceinline__ const bf16* weight_row(const GemmArgs& a, int tn, int u) {
+  constexpr int TN = BN / 2, NB = TN / 32;
+  const int wn = u / TN, nb = (u % TN) >> 5, c = u & 31;
   if constexpr (EPI == EPI_QKV) {
-    // Virtual order: each wave's two 32-column MFMA blocks hold head dims j
-    // and j + head_dim/2, so the rotary pairs meet in one lane.
     const int vs = tn * BN;
     const bf16* base;
     int local;
@@ -46,13 +58,13 @@ __device__ __forceinline__ const bf16* weight_row(const GemmArgs& a, int tn, int
     else if (vs < a.n0 + a.n1) { base = a.B1; local = vs - a.n0; }
     else { base = a.B2; local = vs - a.n0 - a.n1; }
     const int hd = a.head_dim, qpd = hd / 64;
-    const int wn = u >> 6, blk = (u >> 5) & 1, c = u & 31;
-    const int head = wn / qpd;
-    const int dim = (wn % qpd) * 32 + blk * (hd / 2) + c;
+    const int P = wn * (NB / 2) + (nb >> 1), blk = nb & 1;
+    const int head = P / qpd, dim = (P % qpd) * 32 + blk * (hd / 2) + c;
     return base + (size_t)(local + head * hd + dim) * a.K;
   } else if constexpr (EPI == EPI_GATE_UP) {
-    const int f = tn * 64 + (u >> 6) * 32 + (u & 31);
-    return (((u >> 5) & 1) ? a.B1 : a.B0) + (size_t)f * a.K;
+    const int P = wn * (NB / 2) + (nb >> 1);
+    const int f = tn * (BN / 2) + P * 32 + c;
+    return ((nb & 1) ? a.B1 : a.B0) + (size_t)f * a.K;
   } else {
     return a.B0 + (size_t)(tn * BN + u) * a.K;
   }
@@ -60,108 +72,135 @@ __device__ __forceinline__ const bf16* weight_row(const GemmArgs& a, int tn, int
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-template <int EPI>
-__global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2][2][BM * BK * 2];
+template <int EPI, int BM, int BN>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
+  constexpr int TM = BM / 2, TN = BN / 2, MB = TM / 32, NB = TN / 32;
+  constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
+  constexpr int A_LOADS = A_BYTES / 1024 / 4, B_LOADS = BN * BK * 2 / 1024 / 4;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ntm = (a.M + BM - 1) / BM;
   const int total = gridDim.x;
   int bid = blockIdx.x;
   if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
   const int tm = bid % ntm, tn = bid / ntm;
 
-  // Global -> register loader: 4 rows x one 16-byte chunk of A and of B.
-  const int lrow = tid >> 3, lchunk = tid & 7;
-  const bf16* pa[4];
-  const bf16* pb[4];
-  bool oka[4];
+  // Wave-load j of this wave fills tile rows [(wave*LOADS + j)*8, +8); lane l
+  // lands at row l/8, physical chunk l%8, so it fetches logical chunk
+  // (l%8) ^ swz(row).
+  const int lr = lane >> 3;
+  const bf16* pa[A_LOADS];
+  const bf16* pb[B_LOADS];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int row = lrow + 32 * r;
-    const int grow = tm * BM + row;
-    oka[r] = grow < a.M;
-    pa[r] = a.A + (size_t)(oka[r] ? grow : 0) * a.K + lchunk * 8;
-    pb[r] = weight_row<EPI>(a, tn, row) + lchunk * 8;
+  for (int j = 0; j < A_LOADS; ++j) {
+    const int trow = (wave * A_LOADS + j) * 8 + lr;
+    int row = tm * BM + trow;
+    row = row < a.M ? row : a.M - 1;      // rows past M repeat the last row; never stored
+    pa[j] = a.A + (size_t)row * a.K + (((lane & 7) ^ swz(trow)) << 3);
   }
-  i32x4 ra[4], rb[4];
-  auto gload = [&](int k0) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      ra[r] = oka[r] ? *(const i32x4*)(pa[r] + k0) : i32x4{0, 0, 0, 0};
-      rb[r] = *(const i32x4*)(pb[r] + k0);
-    }
-  };
-  auto sstore = [&](int buf) {
+  for (int j = 0; j < B_LOADS; ++j) {
+    const int trow = (wave * B_LOADS + j) * 8 + lr;
+    pb[j] = weight_row<EPI, BN>(a, tn, trow) + (((lane & 7) ^ swz(trow)) << 3);
+  }
+  auto issue = [&](int kt, int slot) {
+    char* base = smem + slot * STAGE;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int off = lds_off(lrow + 32 * r, lchunk);
-      *(i32x4*)(smem[buf][0] + off) = ra[r];
-      *(i32x4*)(smem[buf][1] + off) = rb[r];
-    }
+    for (int j = 0; j < A_LOADS; ++j) load_lds16(pa[j] + kt * BK, base + (wave * A_LOADS + j) * 1024);
+#pragma unroll
+    for (int j = 0; j < B_LOADS; ++j)
+      load_lds16(pb[j] + kt * BK, base + A_BYTES + (wave * B_LOADS + j) * 1024);
   };
 
-  f32x16 acc[2][2];
+  f32x16 acc[MB][NB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < NB; ++j) acc[i][j] = f32x16{};
 
   const int wm = wave >> 1, wn = wave & 1;
+  int arow[MB], brow[NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i) arow[i] = wm * TM + i * 32 + (lane & 31);
+#pragma unroll
+  for (int j = 0; j < NB; ++j) brow[j] = wn * TN + j * 32 + (lane & 31);
+
+  bf16x8 fa[2][MB], fb[2][NB];
+  auto load_frags = [&](const char* st, int ks, int set) {
+    const int chunk = ks * 2 + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+      fa[set][i] = *(const bf16x8*)(st + arow[i] * 128 + ((chunk ^ swz(arow[i])) << 4));
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      fb[set][j] = *(const bf16x8*)(st + A_BYTES + brow[j] * 128 + ((chunk ^ swz(brow[j])) << 4));
+  };
+  auto mfmas = [&](int set) {
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
+  };
+
   const int KT = a.K / BK;
-  gload(0);
-  sstore(0);
+  issue(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  if (KT > 1) issue(1, 1);
+  load_frags(smem, 0, 0);
   for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * BK);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int chunk = ks * 2 + (lane >> 5);
-      bf16x8 af[2], bfr[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        af[i] = *(const bf16x8*)(smem[cur][0] + lds_off(wm * 64 + i * 32 + (lane & 31), chunk));
-        bfr[i] = *(const bf16x8*)(smem[cur][1] + lds_off(wn * 64 + i * 32 + (lane & 31), chunk));
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    const char* st = smem + (kt & 1) * STAGE;
+    load_frags(st, 1, 1);
+    mfmas(0);
+    load_frags(st, 2, 0);
+    mfmas(1);
+    load_frags(st, 3, 1);
+    mfmas(0);
+    if (kt + 1 < KT) {
+      // Stage kt+1 has landed for every wave, and every wave is done reading
+      // stage kt (its last fragments are in registers): refill that slot.
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (kt + 2 < KT) issue(kt + 2, kt & 1);
+      load_frags(smem + ((kt + 1) & 1) * STAGE, 0, 0);
     }
-    if (kt + 1 < KT) sstore(cur ^ 1);
-    __syncthreads();
+    mfmas(1);
   }
 
   // Accumulator layout of a 32x32 block: lane l, element e holds
   // row 8*(e/4) + 4*(l/32) + e%4, column l%32.
   const int c = lane & 31;
-  const int rbase = tm * BM + wm * 64 + 4 * (lane >> 5);
+  const int rbase = tm * BM + wm * TM + 4 * (lane >> 5);
 
   if constexpr (EPI == EPI_RESID) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
           if (row < a.M) {
-            float* px = a.x + (size_t)row * a.N + tn * BN + wn * 64 + j * 32 + c;
+            float* px = a.x + (size_t)row * a.N + tn * BN + wn * TN + j * 32 + c;
             *px += acc[i][j][e];
           }
         }
   } else if constexpr (EPI == EPI_GATE_UP) {
     const int F = a.N / 2;
-    const int f = tn * 64 + wn * 32 + c;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int p = 0; p < NB / 2; ++p) {
+      const int f = tn * (BN / 2) + (wn * (NB / 2) + p) * 32 + c;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-        if (row < a.M) a.act_out[(size_t)row * F + f] = (bf16)(silu(acc[i][0][e]) * acc[i][1][e]);
-      }
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+          if (row < a.M)
+            a.act_out[(size_t)row * F + f] = (bf16)(silu(acc[i][2 * p][e]) * acc[i][2 * p + 1][e]);
+        }
+    }
   } else if constexpr (EPI == EPI_QKV) {
     const int vs = tn * BN;
     int seg, local;
@@ -169,53 +208,58 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
     else if (vs < a.n0 + a.n1) { seg = 1; local = vs - a.n0; }
     else { seg = 2; local = vs - a.n0 - a.n1; }
     const int hd = a.head_dim, qpd = hd / 64, half = hd / 2;
-    const int head = local / hd + wn / qpd;
-    const int fi = (wn % qpd) * 32 + c;             // rotary frequency index, < hd/2
-    const int dim = fi;                             // first element of the pair
     const int nq_hd = a.n0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int p = 0; p < NB / 2; ++p) {
+      const int P = wn * (NB / 2) + p;
+      const int head = local / hd + P / qpd;
+      const int fi = (P % qpd) * 32 + c;           // rotary frequency index = first dim of the pair
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-        if (row >= a.M) continue;
-        float x1 = acc[i][0][e], x2 = acc[i][1][e];
-        if (seg < 2) {
-          const float2 cs = a.rope_cs[(size_t)row * half + fi];
-          const float y1 = x1 * cs.x - x2 * cs.y;
-          const float y2 = x2 * cs.x + x1 * cs.y;
-          x1 = y1;
-          x2 = y2;
-        }
-        if (seg == 0) {
-          bf16* pq = a.q_out + (size_t)row * nq_hd + head * hd + dim;
-          pq[0] = (bf16)x1;
-          pq[half] = (bf16)x2;
-        } else {
-          const TokInfo t = a.toks[row];
-          const SampleInfo s = a.samples[t.sample];
-          const int slot = s.seq_len + t.node;
-          bf16* p = a.kv_pool + s.kv_base +
-                    ((((size_t)a.layer * 2 + (seg - 1)) * a.n_kv_heads + head) * s.cap + slot) * hd +
-                    dim;
-          p[0] = (bf16)x1;
-          p[half] = (bf16)x2;
-        }
-      }
-  } else {  // EPI_ARGMAX
-    const int col0 = tn * BN + wn * 64 + c;
+      for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+        for (int e = 0; e < 16; ++e) {
+          const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+          if (row >= a.M) continue;
+          float x1 = acc[i][2 * p][e], x2 = acc[i][2 * p + 1][e];
+          if (seg < 2) {
+            const float2 cs = a.rope_cs[(size_t)row * half + fi];
+            const float y1 = x1 * cs.x - x2 * cs.y;
+            const float y2 = x2 * cs.x + x1 * cs.y;
+            x1 = y1;
+            x2 = y2;
+          }
+          if (seg == 0) {
+            bf16* pq = a.q_out + (size_t)row * nq_hd + head * hd + fi;
+            pq[0] = (bf16)x1;
+            pq[half] = (bf16)x2;
+          } else {
+            const TokInfo t = a.toks[row];
+            const SampleInfo s = a.samples[t.sample];
+            const int slot = s.seq_len + t.node;
+            bf16* pk = a.kv_pool + s.kv_base +
+                       ((((size_t)a.layer * 2 + (seg - 1)) * a.n_kv_heads + head) * s.cap + slot) * hd +
+                       fi;
+            pk[0] = (bf16)x1;
+            pk[half] = (bf16)x2;
+          }
+        }
+    }
+  } else {  // EPI_ARGMAX: one partial (max, lowest index) per row and wave slab of TN columns
+    const int col0 = tn * BN + wn * TN + c;
+    const int parts = a.N / TN;
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
         float v = acc[i][0][e];
         int idx = col0;
-        const float v2 = acc[i][1][e];
-        if (v2 > v) { v = v2; idx = col0 + 32; }
+#pragma unroll
+        for (int j = 1; j < NB; ++j)
+          if (acc[i][j][e] > v) { v = acc[i][j][e]; idx = col0 + 32 * j; }
         if (a.logits != nullptr && row < a.M) {
-          a.logits[(size_t)row * a.N + col0] = acc[i][0][e];
-          a.logits[(size_t)row * a.N + col0 + 32] = v2;
+#pragma unroll
+          for (int j = 0; j < NB; ++j) a.logits[(size_t)row * a.N + col0 + 32 * j] = acc[i][j][e];
         }
 #pragma unroll
         for (int m = 16; m >= 1; m >>= 1) {
@@ -224,7 +268,6 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
           if (ov > v || (ov == v && oi < idx)) { v = ov; idx = oi; }
         }
         if (c == 0 && row < a.M) {
-          const int parts = a.N / 64;
           a.part_val[(size_t)row * parts + tn * 2 + wn] = v;
           a.part_idx[(size_t)row * parts + tn * 2 + wn] = idx;
         }
@@ -232,20 +275,47 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
   }
 }
 
+template <int EPI, int BM, int BN>
+hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
+  constexpr int SMEM = 2 * (BM + BN) * BK * 2;
+  static bool configured = false;
+  if (!configured) {
+    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  const int grid = ((a.M + BM - 1) / BM) * (a.N / BN);
+  gemm_bf16_kernel<EPI, BM, BN><<<grid, NT, SMEM, s>>>(a);
+  return hipGetLastError();
+}
+
+// 256 x 256 tiles (4 waves of 128 x 128) halve the operand traffic per flop
+// but need enough tiles to cover the 256 CUs; otherwise 128 x 128.  Weight
+// segments (q/k/v) must not straddle a tile.
+bool use_big_tiles(int M, int N, int n0, int n1) {
+  const long big_tiles = (long)((M + 255) / 256) * (N / 256);
+  return N % 256 == 0 && n0 % 256 == 0 && n1 % 256 == 0 && big_tiles >= 384;
+}
+
+template <int EPI>
+hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+  if (use_big_tiles(a.M, a.N, a.n0, a.n1)) return launch_tile<EPI, 256, 256>(a, s);
+  return launch_tile<EPI, 128, 128>(a, s);
+}
+
 }  // namespace
 
+int gemm_parts(int N, int M) { return use_big_tiles(M, N, N, 0) ? N / 128 : N / 64; }
+
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
-  const int ntm = (a.M + BM - 1) / BM;
-  const int ntn = a.N / BN;
-  const dim3 grid(ntm * ntn), block(NT);
   switch (epi) {
-    case EPI_QKV: gemm_bf16_kernel<EPI_QKV><<<grid, block, 0, s>>>(a); break;
-    case EPI_RESID: gemm_bf16_kernel<EPI_RESID><<<grid, block, 0, s>>>(a); break;
-    case EPI_GATE_UP: gemm_bf16_kernel<EPI_GATE_UP><<<grid, block, 0, s>>>(a); break;
-    case EPI_ARGMAX: gemm_bf16_kernel<EPI_ARGMAX><<<grid, block, 0, s>>>(a); break;
+    case EPI_QKV: return launch_epi<EPI_QKV>(a, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, s);
+    case EPI_GATE_UP: return launch_epi<EPI_GATE_UP>(a, s);
+    case EPI_ARGMAX: return launch_epi<EPI_ARGMAX>(a, s);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace spec
