@@ -43,7 +43,7 @@ int hip_fail(hipError_t e, const char* what) {
 
 constexpr size_t kAlign = 256;
 constexpr int kPartCap = 8192;          // split-KV partial tiles per call
-constexpr int kTargetItems = 2048;      // attention work-groups aimed for
+constexpr int kTargetItems = 768;       // attention work-groups aimed for (1 per CU at a time)
 constexpr int kMinChunk = 256;          // keys per split, lower bound
 constexpr int kMaxSplits = 64;          // key ranges per row tile (combine kernel's table)
 
@@ -83,7 +83,8 @@ size_t sample_bytes(const spec_model_config* c, int32_t cap) {
 
 // Workspace carving; every region 256-byte aligned.
 struct WsLayout {
-  size_t blob, toks, anc, rope, x, h, q, o, act, part_o, part_ml, lm_val, lm_idx, argmax, total;
+  size_t blob, toks, anc, rope, x, h, q, o, act, part_o, part_ml, lm_val, lm_idx, argmax, splitk,
+      total;
   size_t blob_bytes;
 };
 
@@ -94,7 +95,8 @@ int64_t max_row_tiles(const spec_model_config* c, int64_t max_batch, int64_t max
 
 WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_tokens) {
   WsLayout L{};
-  const int64_t items = max_row_tiles(c, max_batch, max_tokens) + kPartCap;
+  // attention items: one per row tile and split, then padded per XCD (at most 8x)
+  const int64_t items = 8 * (max_row_tiles(c, max_batch, max_tokens) + kPartCap);
   L.blob_bytes = align_up(max_batch * sizeof(SampleInfo)) + 2 * align_up(max_tokens * 4) +
                  align_up(items * sizeof(AttnItem)) + align_up(kPartCap * sizeof(CombineItem));
   size_t off = 0;
@@ -118,6 +120,7 @@ WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_to
   L.lm_val = take(max_tokens * (size_t)(c->vocab / 64) * 4);
   L.lm_idx = take(max_tokens * (size_t)(c->vocab / 64) * 4);
   L.argmax = take(max_tokens * 4);
+  L.splitk = take(gemm_partial_bytes());
   L.total = off;
   return L;
 }
@@ -370,15 +373,52 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     const int keys = si[b].seq_len + si[b].ntok;
     const int ns = (int)((keys + chunk - 1) / chunk);
     const int tiles = (si[b].ntok * G + 31) / 32;
-    for (int g = 0; g < nkv; ++g)
-      for (int t = 0; t < tiles; ++t) {
-        if (ns > 1) comb.push_back(CombineItem{b, g, t * 32, ns, part, 0, 0, 0});
-        for (int k = 0; k < ns; ++k) {
-          const int k0 = (int)(k * chunk), k1 = (int)std::min<int64_t>(keys, (k + 1) * chunk);
-          items.push_back(AttnItem{b, g, t * 32, k0, k1, ns, ns > 1 ? part + k : 0, 0});
-        }
-        if (ns > 1) part += ns;
+    // Row tiles sharing a key range are consecutive, so they run on one XCD
+    // and read that range from its L2.
+    for (int g = 0; g < nkv; ++g) {
+      for (int t = 0; t < tiles && ns > 1; ++t)
+        comb.push_back(CombineItem{b, g, t * 32, ns, part + t * ns, 0, 0, 0});
+      for (int k = 0; k < ns; ++k) {
+        const int k0 = (int)(k * chunk), k1 = (int)std::min<int64_t>(keys, (k + 1) * chunk);
+        for (int t = 0; t < tiles; ++t)
+          items.push_back(AttnItem{b, g, t * 32, k0, k1, ns, ns > 1 ? part + t * ns + k : 0, 0});
       }
+      if (ns > 1) part += ns * tiles;
+    }
+  }
+  // Longest-first per XCD: the kernel hands XCD x the items [x*per, (x+1)*per)
+  // in order.  Deal the groups of items that share a key range, longest first,
+  // to the XCD with the least work so far; pad every XCD's list to `per` with
+  // empty items (sample -1).
+  {
+    struct Group { size_t first, count; int64_t work; };
+    std::vector<Group> groups;
+    for (size_t i = 0; i < items.size();) {
+      size_t j = i;
+      while (j < items.size() && items[j].sample == items[i].sample && items[j].kvh == items[i].kvh &&
+             items[j].key0 == items[i].key0)
+        ++j;
+      groups.push_back(Group{i, j - i, (int64_t)(items[i].key1 - items[i].key0) * (int64_t)(j - i)});
+      i = j;
+    }
+    std::stable_sort(groups.begin(), groups.end(),
+                     [](const Group& x, const Group& y) { return x.work > y.work; });
+    std::vector<AttnItem> xcd[8];
+    int64_t load[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (const Group& gp : groups) {
+      const int x = (int)(std::min_element(load, load + 8) - load);
+      load[x] += gp.work;
+      xcd[x].insert(xcd[x].end(), items.begin() + gp.first, items.begin() + gp.first + gp.count);
+    }
+    size_t per = 0;
+    for (auto& v : xcd) per = std::max(per, v.size());
+    std::vector<AttnItem> dealt;
+    dealt.reserve(per * 8);
+    for (auto& v : xcd) {
+      dealt.insert(dealt.end(), v.begin(), v.end());
+      dealt.resize(dealt.size() + (per - v.size()), AttnItem{-1, 0, 0, 0, 0, 1, 0, 0});
+    }
+    items.swap(dealt);
   }
 
   // ---- one upload of the per-call descriptors ----
@@ -429,6 +469,7 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
   ga.n_kv_heads = nkv;
   ga.head_dim = hd;
   ga.rope_cs = d_rope;
+  ga.partial = (float*)(ws + ly.splitk);
   AttnArgs aa{};
   aa.q = d_q;
   aa.kv_pool = kv->pool;

@@ -6,16 +6,20 @@
 // S_b + t, exactly its ancestors t (itself included), given as a bitmask.
 //
 // One work-group takes a tile of 32 query rows and a key range [key0, key1)
-// (split-KV: long caches are cut into ranges processed in parallel and merged
-// by the combine kernel).  Per step it stages 128 keys of K (row-major,
-// chunk-swizzled) and V (transposed, [dim][key]) in LDS with coalesced 16-byte
-// loads; wave w handles keys [32w, 32w+32) of the step:
+// of their cache (split-KV: long caches are cut into ranges processed in
+// parallel and merged by the combine kernel).  The range is cut into blocks of
+// 32 keys dealt round-robin to the 4 waves; each wave is an independent
+// streaming worker with a private LDS ring that it fills itself with
+// global_load_lds_dwordx4 (K and V rows copied verbatim, K chunk-swizzled), so
+// the key loop needs no work-group barrier, only the wave's own vmcnt waits.
+// Per 32-key block:
 //
-//   S^T (32 keys x 32 rows) = K . Q^T   v_mfma_f32_32x32x16_bf16, A = K from LDS
+//   S^T (32 keys x 32 rows) = K . Q^T   v_mfma_f32_32x32x16_bf16, A = K (LDS)
 //   online softmax per row              each lane owns one row (16 of its keys,
 //                                       the other 16 in lane ^ 32)
-//   O^T (dims x 32 rows) += V^T . P^T   A = V^T from LDS, B = P straight from
-//                                       the S^T accumulator registers
+//   O^T (dims x 32 rows) += V^T . P^T   A = V^T gathered from the row-major V
+//                                       rows in LDS, B = P straight from the
+//                                       S^T accumulator registers
 //
 // Computing the transposed products keeps a row's softmax state and its
 // output column in the same lane, so rescaling needs no data movement.  At the
@@ -28,31 +32,59 @@ namespace spec {
 
 namespace {
 
-constexpr int KB = 128;       // keys per step
-constexpr int NT = 256;
+constexpr int NT = 256, KBLK = 32;
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void load_lds16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
+}
 
 template <int HD>
-struct AttnSmem {
-  static constexpr int VT_STRIDE = KB + 4;                       // bf16 per V^T row
-  static constexpr int K_BYTES = KB * HD * 2;
-  static constexpr int VT_BYTES = HD * VT_STRIDE * 2;
-  static constexpr int O_STRIDE = HD + 1;                        // floats per merge row
+struct AttnCfg {
+  static constexpr int ROW = HD * 2;                    // bytes per K or V row
+  static constexpr int NST = HD == 128 ? 2 : 4;         // ring stages per wave
+  static constexpr int KV_BYTES = KBLK * ROW;           // one block of K (or V)
+  static constexpr int STAGE = 2 * KV_BYTES;
+  static constexpr int WAVE_RING = NST * STAGE;         // 32 KB per wave
+  static constexpr int LOADS = KV_BYTES / 1024;         // wave-loads for K (and for V)
+  static constexpr int ROWS_PER_LOAD = 1024 / ROW;
+  static constexpr int O_STRIDE = HD + 1;               // floats per merge row
   static constexpr int MERGE_BYTES = 4 * 32 * O_STRIDE * 4 + 4 * 32 * 2 * 4;
-  static constexpr int BYTES = (K_BYTES + VT_BYTES) > MERGE_BYTES ? (K_BYTES + VT_BYTES) : MERGE_BYTES;
+  static constexpr int SMEM = (4 * WAVE_RING) > MERGE_BYTES ? (4 * WAVE_RING) : MERGE_BYTES;
 };
 
+// Physical 16-byte chunk of logical chunk c in K row `key`: 16 consecutive
+// rows reading one logical chunk hit 16 distinct 16-byte bank groups.
 template <int HD>
-__global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
-  using SM = AttnSmem<HD>;
-  constexpr int DC = HD / 8;                  // 16-byte chunks per row
-  constexpr int KLOADS = KB * DC / NT;        // K chunks per thread per step
-  constexpr int VPAIRS = (KB / 4) * DC / NT;  // (4-key group, chunk) pairs per thread
-  constexpr int NB = HD / 32;                 // 32-dim output blocks
-  __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
-  char* k_lds = smem;
-  bf16* vt_lds = (bf16*)(smem + SM::K_BYTES);
+__device__ __forceinline__ int kswz(int key) {
+  return HD == 128 ? (key & 15) : ((key >> 1) & 7);
+}
 
-  const AttnItem it = a.items[blockIdx.x];
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  else if constexpr (N == 24) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+  else static_assert(N < 0, "unsupported vmcnt");
+}
+
+template <int HD>
+__global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
+  using C = AttnCfg<HD>;
+  constexpr int DC = HD / 8;                  // 16-byte chunks per row
+  constexpr int NB = HD / 32;                 // 32-dim output blocks
+  constexpr int LPS = 2 * C::LOADS;           // wave-loads per stage
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+
+  // Items are dealt round-robin over the 8 XCDs; remap so that consecutive
+  // items (the row tiles sharing one key range) run on one XCD.
+  const int per_xcd = gridDim.x >> 3;
+  const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (item >= a.n_items) return;
+  const AttnItem it = a.items[item];
+  if (it.sample < 0) return;          // padding of a shorter per-XCD list
   const SampleInfo si = a.samples[it.sample];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r = lane & 31, h = lane >> 5;
@@ -75,6 +107,28 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
   const size_t head_stride = (size_t)si.cap * HD;
   const bf16* kbase = a.kv_pool + si.kv_base + ((size_t)a.layer * 2 * a.n_kv_heads + it.kvh) * head_stride;
   const bf16* vbase = kbase + (size_t)a.n_kv_heads * head_stride;
+  char* ring = smem + w * C::WAVE_RING;
+
+  // Blocks of this wave: w, w+4, w+8, ... of the item's range.
+  const int nblk = (it.key1 - it.key0 + KBLK - 1) / KBLK;
+  const int mine = nblk > w ? (nblk - w + 3) / 4 : 0;
+
+  // Lane l of wave-load j copies row (j*ROWS_PER_LOAD + l / DC) of the block,
+  // 16-byte chunk l % DC (physical); keys past the range repeat the last key,
+  // whose scores are masked.
+  const int lrow = lane / DC, lch = lane % DC;
+  auto issue = [&](int t, int slot) {
+    const int kb = it.key0 + (w + 4 * t) * KBLK;
+    char* st = ring + slot * C::STAGE;
+#pragma unroll
+    for (int j = 0; j < C::LOADS; ++j) {
+      const int row = j * C::ROWS_PER_LOAD + lrow;
+      int key = kb + row;
+      key = key < it.key1 ? key : it.key1 - 1;
+      load_lds16(kbase + (size_t)key * HD + ((lch ^ kswz<HD>(row)) << 3), st + j * 1024);
+      load_lds16(vbase + (size_t)key * HD + (lch << 3), st + C::KV_BYTES + j * 1024);
+    }
+  };
 
   const float sl2 = 1.4426950408889634f / sqrtf((float)HD);   // log2(e)/sqrt(d)
   float m_run = -INFINITY, l_run = 0.f;
@@ -82,71 +136,52 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < NB; ++i) o[i] = f32x16{};
 
-  i32x4 kreg[KLOADS];
-  i32x4 vreg[VPAIRS][4];
-  auto gload = [&](int kb) {
 #pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int q = tid + NT * i, key = q / DC, c = q % DC;
-      kreg[i] = (kb + key < it.key1) ? *(const i32x4*)(kbase + (size_t)(kb + key) * HD + c * 8)
-                                     : i32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int i = 0; i < VPAIRS; ++i) {
-      const int p = tid + NT * i, kg = p / DC, c = p % DC;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int key = kb + kg * 4 + j;
-        vreg[i][j] = (key < it.key1) ? *(const i32x4*)(vbase + (size_t)key * HD + c * 8)
-                                     : i32x4{0, 0, 0, 0};
-      }
-    }
-  };
-  auto sstore = [&]() {
-#pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int q = tid + NT * i, key = q / DC, c = q % DC;
-      *(i32x4*)(k_lds + key * HD * 2 + ((c ^ (key & 7)) << 4)) = kreg[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VPAIRS; ++i) {
-      const int p = tid + NT * i, kg = p / DC, c = p % DC;
-      const bf16x8 v0 = __builtin_bit_cast(bf16x8, vreg[i][0]);
-      const bf16x8 v1 = __builtin_bit_cast(bf16x8, vreg[i][1]);
-      const bf16x8 v2 = __builtin_bit_cast(bf16x8, vreg[i][2]);
-      const bf16x8 v3 = __builtin_bit_cast(bf16x8, vreg[i][3]);
-#pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        const bf16x4 t = {v0[dd], v1[dd], v2[dd], v3[dd]};
-        *(bf16x4*)(vt_lds + (c * 8 + dd) * SM::VT_STRIDE + kg * 4) = t;
-      }
-    }
-  };
+  for (int t = 0; t < C::NST - 1; ++t)
+    if (t < mine) issue(t, t);
 
-  if (it.key0 < it.key1) gload(it.key0);
-  for (int kb = it.key0; kb < it.key1; kb += KB) {
-    __syncthreads();                       // previous step's LDS reads are done
-    sstore();
-    __syncthreads();
-    if (kb + KB < it.key1) gload(kb + KB); // next step's loads overlap this step's math
-
-    // S^T = K . Q^T for keys [32w, 32w+32) of this step.
-    f32x16 s = f32x16{};
-    const int krow = w * 32 + r;
-#pragma unroll
-    for (int ks = 0; ks < HD / 16; ++ks) {
-      const bf16x8 kf = *(const bf16x8*)(k_lds + krow * HD * 2 + (((2 * ks + h) ^ (krow & 7)) << 4));
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
+  for (int t = 0; t < mine; ++t) {
+    // Keep NST-1 blocks in flight: issue block t+NST-1 into the slot of block
+    // t-1 (consumed in the previous iteration), then wait for block t.
+    if (t + C::NST - 1 < mine) {
+      issue(t + C::NST - 1, (t + C::NST - 1) % C::NST);
+      wait_vm<LPS * (C::NST - 1)>();
+    } else {
+      wait_vm<0>();
     }
-    // Element e of this lane: key kb + 32w + 8*(e/4) + 4h + e%4 of row r.
+    const char* st = ring + (t % C::NST) * C::STAGE;
+    const bf16* vt = (const bf16*)(st + C::KV_BYTES);
+    const int kb = it.key0 + (w + 4 * t) * KBLK;
+
+    // S^T = K . Q^T for the 32 keys of this block (two independent chains).
+    f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ks += 2) {
+      const bf16x8 k0 = *(const bf16x8*)(st + r * C::ROW + (((2 * ks + h) ^ kswz<HD>(r)) << 4));
+      const bf16x8 k1 = *(const bf16x8*)(st + r * C::ROW + (((2 * ks + 2 + h) ^ kswz<HD>(r)) << 4));
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks + 1], s1, 0, 0, 0);
+    }
+    f32x16 s = s0 + s1;
+    // Element e of this lane: key kb + 8*(e/4) + 4h + e%4 of row r.  Blocks
+    // wholly inside the committed prefix need no mask.
     float smax = -INFINITY;
+    if (kb + KBLK <= si.seq_len && kb + KBLK <= it.key1) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = kb + w * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-      const int t = key - si.seq_len;
-      const bool vis = key < it.key1 && (t < 0 || ((anc_row >> t) & 1ull));
-      s[e] = vis ? s[e] * sl2 : -INFINITY;
-      smax = fmaxf(smax, s[e]);
+      for (int e = 0; e < 16; ++e) {
+        s[e] *= sl2;
+        smax = fmaxf(smax, s[e]);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = kb + 8 * (e >> 2) + 4 * h + (e & 3);
+        const int tt = key - si.seq_len;
+        const bool anc_bit = (anc_row >> (tt & 63)) & 1ull;
+        const bool vis = (key < it.key1) & ((tt < 0) | anc_bit);
+        s[e] = vis ? s[e] * sl2 : -INFINITY;
+        smax = fmaxf(smax, s[e]);
+      }
     }
     smax = fmaxf(smax, __shfl_xor(smax, 32));
     const float m_new = fmaxf(m_run, smax);
@@ -168,14 +203,14 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
     // O^T += V^T . P^T.  Register slot j of k-step st (this lane's half h)
     // carries key 16*st + 8*(j/4) + 4h + j%4, matching the S^T layout.
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
+    for (int kst = 0; kst < 2; ++kst) {
 #pragma unroll
       for (int i = 0; i < NB; ++i) {
-        const bf16* vp = vt_lds + (i * 32 + r) * SM::VT_STRIDE + w * 32 + 16 * st + 4 * h;
-        const bf16x4 lo = *(const bf16x4*)vp;
-        const bf16x4 hi = *(const bf16x4*)(vp + 8);
-        const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[st], o[i], 0, 0, 0);
+        const bf16* vp = vt + (16 * kst + 4 * h) * HD + i * 32 + r;
+        bf16x8 vf;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) vf[j] = vp[((j >> 2) * 8 + (j & 3)) * HD];
+        o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kst], o[i], 0, 0, 0);
       }
     }
   }
@@ -184,7 +219,7 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
   // Merge the four waves' (m, l, O) through LDS.
   __syncthreads();
   float* o_sh = (float*)smem;
-  float* ml_sh = o_sh + 4 * 32 * SM::O_STRIDE;
+  float* ml_sh = o_sh + 4 * 32 * C::O_STRIDE;
   if (h == 0) {
     ml_sh[(w * 32 + r) * 2] = m_run;
     ml_sh[(w * 32 + r) * 2 + 1] = l_run;
@@ -194,7 +229,7 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int d = i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-      o_sh[(w * 32 + r) * SM::O_STRIDE + d] = o[i][e];
+      o_sh[(w * 32 + r) * C::O_STRIDE + d] = o[i][e];
     }
   __syncthreads();
 
@@ -211,7 +246,7 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_kernel(AttnArgs a) {
     for (int ww = 0; ww < 4; ++ww) {
       const float mw = ml_sh[(ww * 32 + row) * 2];
       const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
-      O += f * o_sh[(ww * 32 + row) * SM::O_STRIDE + d];
+      O += f * o_sh[(ww * 32 + row) * C::O_STRIDE + d];
       L += f * ml_sh[(ww * 32 + row) * 2 + 1];
     }
     if (it.nsplit == 1) {
@@ -267,20 +302,29 @@ __global__ __launch_bounds__(HD) void attention_combine_kernel(AttnArgs a) {
   a.out[(size_t)(si.tok0 + nd) * a.n_heads * HD + hq * HD + d] = (bf16)(O * inv_l);
 }
 
+template <int HD>
+hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
+  constexpr int SMEM = AttnCfg<HD>::SMEM;
+  static bool configured = false;
+  if (!configured) {
+    const hipError_t e = hipFuncSetAttribute((const void*)tree_attention_kernel<HD>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  const int grid = (a.n_items + 7) / 8 * 8;
+  tree_attention_kernel<HD><<<grid, NT, SMEM, s>>>(a);
+  if (a.n_comb) attention_combine_kernel<HD><<<dim3(a.n_comb, 32), HD, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.n_items == 0) return hipSuccess;
-  if (a.head_dim == 128) {
-    tree_attention_kernel<128><<<a.n_items, NT, 0, s>>>(a);
-    if (a.n_comb) attention_combine_kernel<128><<<dim3(a.n_comb, 32), 128, 0, s>>>(a);
-  } else if (a.head_dim == 64) {
-    tree_attention_kernel<64><<<a.n_items, NT, 0, s>>>(a);
-    if (a.n_comb) attention_combine_kernel<64><<<dim3(a.n_comb, 32), 64, 0, s>>>(a);
-  } else {
-    return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  if (a.head_dim == 128) return launch_hd<128>(a, s);
+  if (a.head_dim == 64) return launch_hd<64>(a, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace spec

@@ -80,12 +80,18 @@ struct GemmArgs {
   float* part_val;        // [M][gemm_parts(N, M)]
   int32_t* part_idx;
   float* logits;          // optional [M][N]
+  // Split-K scratch (gemm_partial_bytes() bytes; NULL disables splitting) and
+  // the split count the launcher picked.
+  float* partial;
+  int ksplit;
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 // Number of (max, index) partials per row the EPI_ARGMAX launch for an
 // [M x N] product writes.
 int gemm_parts(int N, int M);
+// Bytes of split-K partial storage launch_gemm may use through GemmArgs::partial.
+size_t gemm_partial_bytes();
 
 struct AttnArgs {
   const bf16* q;            // [N][n_heads*head_dim]

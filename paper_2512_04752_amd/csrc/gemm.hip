@@ -26,6 +26,13 @@
 // Work-groups are dealt round-robin over the 8 XCDs; the tile order is
 // remapped so that the M tiles sharing one weight tile run on one XCD and hit
 // its L2 instead of HBM.
+//
+// Products with too few output tiles to fill the 256 CUs (few rows, narrow
+// outputs) split K: each split writes its fp32 tile to a partial buffer and a
+// second kernel sums the splits in a fixed order (bitwise reproducible) and
+// applies the same epilogue.
+#include <algorithm>
+
 #include "common.h"
 
 namespace spec {
@@ -33,6 +40,7 @@ namespace spec {
 namespace {
 
 constexpr int BK = 64, NT = 256;
+constexpr size_t kPartialCap = 64ull << 20;   // bytes of split-K partials (workspace)
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -44,8 +52,8 @@ __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
 // Virtual-column mapping.  Column u of an output tile belongs to wave
 // wn = u / TN, MFMA block nb = (u % TN) / 32, lane column c = u % 32.  For
-// EPI_QKV and EPI_GATE_UP, blocks (2p, 2p+1) of a wave form pair p: rotary
-// partners (dims j, j + d/2) or (gate, up) of the same feature.
+// EPI_QKV and EPI_GATE_UP, blocks (2p, 2p+1) of a wave form pair P = wn*NB/2+p
+// of the tile: rotary partners (dims j, j + d/2) or (gate, up) of one feature.
 template <int EPI, int BN>
 __device__ __forceinline__ const bf16* weight_row(const GemmArgs& a, int tn, int u) {
   constexpr int TN = BN / 2, NB = TN / 32;
@@ -72,6 +80,48 @@ __device__ __forceinline__ const bf16* weight_row(const GemmArgs& a, int tn, int
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
+// Pair epilogues: (x1, x2) are the two members of pair P of tile tn, lane
+// column c, output row `row`.
+template <int BN>
+__device__ __forceinline__ void epi_qkv(const GemmArgs& a, int row, int tn, int P, int c, float x1,
+                                        float x2) {
+  const int vs = tn * BN;
+  int seg, local;
+  if (vs < a.n0) { seg = 0; local = vs; }
+  else if (vs < a.n0 + a.n1) { seg = 1; local = vs - a.n0; }
+  else { seg = 2; local = vs - a.n0 - a.n1; }
+  const int hd = a.head_dim, qpd = hd / 64, half = hd / 2;
+  const int head = local / hd + P / qpd;
+  const int fi = (P % qpd) * 32 + c;           // rotary frequency index = first dim of the pair
+  if (seg < 2) {
+    const float2 cs = a.rope_cs[(size_t)row * half + fi];
+    const float y1 = x1 * cs.x - x2 * cs.y;
+    const float y2 = x2 * cs.x + x1 * cs.y;
+    x1 = y1;
+    x2 = y2;
+  }
+  if (seg == 0) {
+    bf16* pq = a.q_out + (size_t)row * a.n0 + head * hd + fi;
+    pq[0] = (bf16)x1;
+    pq[half] = (bf16)x2;
+  } else {
+    const TokInfo t = a.toks[row];
+    const SampleInfo s = a.samples[t.sample];
+    const int slot = s.seq_len + t.node;
+    bf16* pk = a.kv_pool + s.kv_base +
+               ((((size_t)a.layer * 2 + (seg - 1)) * a.n_kv_heads + head) * s.cap + slot) * hd + fi;
+    pk[0] = (bf16)x1;
+    pk[half] = (bf16)x2;
+  }
+}
+
+template <int BN>
+__device__ __forceinline__ void epi_gate_up(const GemmArgs& a, int row, int tn, int P, int c,
+                                            float g, float u) {
+  const int f = tn * (BN / 2) + P * 32 + c;
+  a.act_out[(size_t)row * (a.N / 2) + f] = (bf16)(silu(g) * u);
+}
+
 template <int EPI, int BM, int BN>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int TM = BM / 2, TN = BN / 2, MB = TM / 32, NB = TN / 32;
@@ -81,10 +131,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ntm = (a.M + BM - 1) / BM;
+  const int tiles = ntm * (a.N / BN);
   const int total = gridDim.x;
   int bid = blockIdx.x;
   if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
-  const int tm = bid % ntm, tn = bid / ntm;
+  const int tile = bid % tiles, split = bid / tiles;
+  const int tm = tile % ntm, tn = tile / ntm;
+  const int KT = a.K / BK / a.ksplit;            // K steps of this split
+  const int k_off = split * KT * BK;
 
   // Wave-load j of this wave fills tile rows [(wave*LOADS + j)*8, +8); lane l
   // lands at row l/8, physical chunk l%8, so it fetches logical chunk
@@ -97,12 +151,12 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
     const int trow = (wave * A_LOADS + j) * 8 + lr;
     int row = tm * BM + trow;
     row = row < a.M ? row : a.M - 1;      // rows past M repeat the last row; never stored
-    pa[j] = a.A + (size_t)row * a.K + (((lane & 7) ^ swz(trow)) << 3);
+    pa[j] = a.A + (size_t)row * a.K + k_off + (((lane & 7) ^ swz(trow)) << 3);
   }
 #pragma unroll
   for (int j = 0; j < B_LOADS; ++j) {
     const int trow = (wave * B_LOADS + j) * 8 + lr;
-    pb[j] = weight_row<EPI, BN>(a, tn, trow) + (((lane & 7) ^ swz(trow)) << 3);
+    pb[j] = weight_row<EPI, BN>(a, tn, trow) + k_off + (((lane & 7) ^ swz(trow)) << 3);
   }
   auto issue = [&](int kt, int slot) {
     char* base = smem + slot * STAGE;
@@ -144,7 +198,6 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
   };
 
-  const int KT = a.K / BK;
   issue(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -174,7 +227,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   const int c = lane & 31;
   const int rbase = tm * BM + wm * TM + 4 * (lane >> 5);
 
-  if constexpr (EPI == EPI_RESID) {
+  if (a.ksplit > 1) {
+    // Raw fp32 tile of this split, virtual column order.
+    float* out = a.partial + (size_t)split * a.M * a.N + tn * BN + wn * TN + c;
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
@@ -182,68 +237,46 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-          if (row < a.M) {
-            float* px = a.x + (size_t)row * a.N + tn * BN + wn * TN + j * 32 + c;
-            *px += acc[i][j][e];
-          }
+          if (row < a.M) out[(size_t)row * a.N + j * 32] = acc[i][j][e];
         }
-  } else if constexpr (EPI == EPI_GATE_UP) {
-    const int F = a.N / 2;
+    return;
+  }
+
+  if constexpr (EPI == EPI_RESID) {
+    // Read a whole 32x32 block of the residual before writing any of it, so
+    // the 16 loads per lane are in flight together.
+    float* xcol = a.x + tn * BN + wn * TN + c;
 #pragma unroll
-    for (int p = 0; p < NB / 2; ++p) {
-      const int f = tn * (BN / 2) + (wn * (NB / 2) + p) * 32 + c;
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
+      for (int j = 0; j < NB; ++j) {
+        float xv[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-          if (row < a.M)
-            a.act_out[(size_t)row * F + f] = (bf16)(silu(acc[i][2 * p][e]) * acc[i][2 * p + 1][e]);
+          xv[e] = row < a.M ? xcol[(size_t)row * a.N + j * 32] : 0.f;
         }
-    }
-  } else if constexpr (EPI == EPI_QKV) {
-    const int vs = tn * BN;
-    int seg, local;
-    if (vs < a.n0) { seg = 0; local = vs; }
-    else if (vs < a.n0 + a.n1) { seg = 1; local = vs - a.n0; }
-    else { seg = 2; local = vs - a.n0 - a.n1; }
-    const int hd = a.head_dim, qpd = hd / 64, half = hd / 2;
-    const int nq_hd = a.n0;
 #pragma unroll
-    for (int p = 0; p < NB / 2; ++p) {
-      const int P = wn * (NB / 2) + p;
-      const int head = local / hd + P / qpd;
-      const int fi = (P % qpd) * 32 + c;           // rotary frequency index = first dim of the pair
+        for (int e = 0; e < 16; ++e) {
+          const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+          if (row < a.M) xcol[(size_t)row * a.N + j * 32] = xv[e] + acc[i][j][e];
+        }
+      }
+  } else if constexpr (EPI == EPI_GATE_UP || EPI == EPI_QKV) {
+#pragma unroll
+    for (int p = 0; p < NB / 2; ++p)
 #pragma unroll
       for (int i = 0; i < MB; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
           if (row >= a.M) continue;
-          float x1 = acc[i][2 * p][e], x2 = acc[i][2 * p + 1][e];
-          if (seg < 2) {
-            const float2 cs = a.rope_cs[(size_t)row * half + fi];
-            const float y1 = x1 * cs.x - x2 * cs.y;
-            const float y2 = x2 * cs.x + x1 * cs.y;
-            x1 = y1;
-            x2 = y2;
-          }
-          if (seg == 0) {
-            bf16* pq = a.q_out + (size_t)row * nq_hd + head * hd + fi;
-            pq[0] = (bf16)x1;
-            pq[half] = (bf16)x2;
-          } else {
-            const TokInfo t = a.toks[row];
-            const SampleInfo s = a.samples[t.sample];
-            const int slot = s.seq_len + t.node;
-            bf16* pk = a.kv_pool + s.kv_base +
-                       ((((size_t)a.layer * 2 + (seg - 1)) * a.n_kv_heads + head) * s.cap + slot) * hd +
-                       fi;
-            pk[0] = (bf16)x1;
-            pk[half] = (bf16)x2;
-          }
+          const int P = wn * (NB / 2) + p;
+          if constexpr (EPI == EPI_QKV)
+            epi_qkv<BN>(a, row, tn, P, c, acc[i][2 * p][e], acc[i][2 * p + 1][e]);
+          else
+            epi_gate_up<BN>(a, row, tn, P, c, acc[i][2 * p][e], acc[i][2 * p + 1][e]);
         }
-    }
   } else {  // EPI_ARGMAX: one partial (max, lowest index) per row and wave slab of TN columns
     const int col0 = tn * BN + wn * TN + c;
     const int parts = a.N / TN;
@@ -275,6 +308,33 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   }
 }
 
+// Sum the K splits of a 128 x 128-tiled product in split order and apply the
+// epilogue.  Thread (row, group g of 64 virtual columns, lane column c) owns
+// virtual columns g*64 + c and g*64 + 32 + c: one rotary / gate-up pair (tile
+// g/2, pair g%2), or two residual columns.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int half_n = a.N / 2;
+  if (idx >= (size_t)a.M * half_n) return;
+  const int row = (int)(idx / half_n), rem = (int)(idx % half_n);
+  const int g = rem >> 5, c = rem & 31;
+  const size_t base = (size_t)row * a.N + g * 64 + c;
+  float x1 = 0.f, x2 = 0.f;
+  for (int s = 0; s < a.ksplit; ++s) {
+    x1 += a.partial[(size_t)s * a.M * a.N + base];
+    x2 += a.partial[(size_t)s * a.M * a.N + base + 32];
+  }
+  if constexpr (EPI == EPI_RESID) {
+    a.x[base] += x1;
+    a.x[base + 32] += x2;
+  } else if constexpr (EPI == EPI_QKV) {
+    epi_qkv<128>(a, row, g >> 1, g & 1, c, x1, x2);
+  } else if constexpr (EPI == EPI_GATE_UP) {
+    epi_gate_up<128>(a, row, g >> 1, g & 1, c, x1, x2);
+  }
+}
+
 template <int EPI, int BM, int BN>
 hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   constexpr int SMEM = 2 * (BM + BN) * BK * 2;
@@ -285,8 +345,12 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     configured = true;
   }
-  const int grid = ((a.M + BM - 1) / BM) * (a.N / BN);
+  const int grid = ((a.M + BM - 1) / BM) * (a.N / BN) * a.ksplit;
   gemm_bf16_kernel<EPI, BM, BN><<<grid, NT, SMEM, s>>>(a);
+  if (a.ksplit > 1) {
+    const size_t threads = (size_t)a.M * (a.N / 2);
+    splitk_reduce_kernel<EPI><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
+  }
   return hipGetLastError();
 }
 
@@ -298,15 +362,33 @@ bool use_big_tiles(int M, int N, int n0, int n1) {
   return N % 256 == 0 && n0 % 256 == 0 && n1 % 256 == 0 && big_tiles >= 384;
 }
 
+// K splits for a 128 x 128-tiled product: enough work-groups for about two
+// per CU, at least 4 K steps per split, partials within the workspace area.
+int choose_splits(int epi, int M, int N, int K) {
+  if (epi == EPI_ARGMAX) return 1;
+  const long tiles = (long)((M + 127) / 128) * (N / 128);
+  if (tiles >= 384) return 1;
+  int s = (int)std::min<long>(8, (512 + tiles - 1) / tiles);
+  const int kt = K / BK;
+  while (s > 1 && (kt % s != 0 || kt / s < 4 || (size_t)s * M * N * 4 > kPartialCap)) --s;
+  return s;
+}
+
 template <int EPI>
-hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  if (use_big_tiles(a.M, a.N, a.n0, a.n1)) return launch_tile<EPI, 256, 256>(a, s);
+hipError_t launch_epi(GemmArgs a, hipStream_t s) {
+  if (use_big_tiles(a.M, a.N, a.n0, a.n1)) {
+    a.ksplit = 1;
+    return launch_tile<EPI, 256, 256>(a, s);
+  }
+  a.ksplit = a.partial ? choose_splits(EPI, a.M, a.N, a.K) : 1;
   return launch_tile<EPI, 128, 128>(a, s);
 }
 
 }  // namespace
 
 int gemm_parts(int N, int M) { return use_big_tiles(M, N, N, 0) ? N / 128 : N / 64; }
+
+size_t gemm_partial_bytes() { return kPartialCap; }
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
   switch (epi) {
