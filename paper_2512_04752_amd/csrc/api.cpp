@@ -98,7 +98,8 @@ WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_to
   // attention items: one per row tile and split, then padded per XCD (at most 8x)
   const int64_t items = 8 * (max_row_tiles(c, max_batch, max_tokens) + kPartCap);
   L.blob_bytes = align_up(max_batch * sizeof(SampleInfo)) + 2 * align_up(max_tokens * 4) +
-                 align_up(items * sizeof(AttnItem)) + align_up(kPartCap * sizeof(CombineItem));
+                 align_up(items * sizeof(AttnItem)) + kAlign +      // narrow + wide lists
+                 align_up(kPartCap * sizeof(CombineItem));
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -365,7 +366,11 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     return slots;
   };
   while (slots_for(chunk) > kPartCap) chunk *= 2;
-  std::vector<AttnItem> items;
+  // Work items.  A (sample, kv head) with at most 32 query rows gets narrow
+  // items (one 32-row tile); more rows get wide items of 128 rows (4 tiles),
+  // which read each key range once for all their rows.  Split key ranges
+  // write their partial states to per-tile slots part + tile * ns + split.
+  std::vector<AttnItem> items, wide;
   std::vector<CombineItem> comb;
   items.reserve(row_tiles * 2);
   int part = 0;
@@ -373,32 +378,33 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     const int keys = si[b].seq_len + si[b].ntok;
     const int ns = (int)((keys + chunk - 1) / chunk);
     const int tiles = (si[b].ntok * G + 31) / 32;
-    // Row tiles sharing a key range are consecutive, so they run on one XCD
-    // and read that range from its L2.
     for (int g = 0; g < nkv; ++g) {
       for (int t = 0; t < tiles && ns > 1; ++t)
         comb.push_back(CombineItem{b, g, t * 32, ns, part + t * ns, 0, 0, 0});
       for (int k = 0; k < ns; ++k) {
         const int k0 = (int)(k * chunk), k1 = (int)std::min<int64_t>(keys, (k + 1) * chunk);
-        for (int t = 0; t < tiles; ++t)
-          items.push_back(AttnItem{b, g, t * 32, k0, k1, ns, ns > 1 ? part + t * ns + k : 0, 0});
+        if (tiles == 1)
+          items.push_back(AttnItem{b, g, 0, k0, k1, ns, ns > 1 ? part + k : 0, 0});
+        else
+          for (int rg = 0; rg < (tiles + 3) / 4; ++rg)
+            wide.push_back(AttnItem{b, g, rg * 128, k0, k1, ns, ns > 1 ? part + rg * 4 * ns + k : 0, 0});
       }
       if (ns > 1) part += ns * tiles;
     }
   }
-  // Longest-first per XCD: the kernel hands XCD x the items [x*per, (x+1)*per)
-  // in order.  Deal the groups of items that share a key range, longest first,
-  // to the XCD with the least work so far; pad every XCD's list to `per` with
-  // empty items (sample -1).
-  {
+  // Longest-first per XCD: a kernel hands XCD x the items [x*per, (x+1)*per)
+  // in order.  Deal the groups of items that share a key range (adjacent, so
+  // they meet in one XCD's L2), longest first, to the XCD with the least work
+  // so far; pad every XCD's list to `per` with empty items (sample -1).
+  auto deal = [](std::vector<AttnItem>& list) {
     struct Group { size_t first, count; int64_t work; };
     std::vector<Group> groups;
-    for (size_t i = 0; i < items.size();) {
+    for (size_t i = 0; i < list.size();) {
       size_t j = i;
-      while (j < items.size() && items[j].sample == items[i].sample && items[j].kvh == items[i].kvh &&
-             items[j].key0 == items[i].key0)
+      while (j < list.size() && list[j].sample == list[i].sample && list[j].kvh == list[i].kvh &&
+             list[j].key0 == list[i].key0)
         ++j;
-      groups.push_back(Group{i, j - i, (int64_t)(items[i].key1 - items[i].key0) * (int64_t)(j - i)});
+      groups.push_back(Group{i, j - i, (int64_t)(list[i].key1 - list[i].key0) * (int64_t)(j - i)});
       i = j;
     }
     std::stable_sort(groups.begin(), groups.end(),
@@ -408,7 +414,7 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     for (const Group& gp : groups) {
       const int x = (int)(std::min_element(load, load + 8) - load);
       load[x] += gp.work;
-      xcd[x].insert(xcd[x].end(), items.begin() + gp.first, items.begin() + gp.first + gp.count);
+      xcd[x].insert(xcd[x].end(), list.begin() + gp.first, list.begin() + gp.first + gp.count);
     }
     size_t per = 0;
     for (auto& v : xcd) per = std::max(per, v.size());
@@ -418,21 +424,25 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
       dealt.insert(dealt.end(), v.begin(), v.end());
       dealt.resize(dealt.size() + (per - v.size()), AttnItem{-1, 0, 0, 0, 0, 1, 0, 0});
     }
-    items.swap(dealt);
-  }
+    list.swap(dealt);
+  };
+  deal(items);
+  deal(wide);
 
   // ---- one upload of the per-call descriptors ----
   const size_t o_si = 0;
   const size_t o_tok = align_up(batch * sizeof(SampleInfo));
   const size_t o_par = o_tok + align_up((size_t)N * 4);
   const size_t o_items = o_par + align_up((size_t)N * 4);
-  const size_t o_comb = o_items + align_up(items.size() * sizeof(AttnItem));
+  const size_t o_wide = o_items + align_up(items.size() * sizeof(AttnItem));
+  const size_t o_comb = o_wide + align_up(wide.size() * sizeof(AttnItem));
   const size_t blob_bytes = o_comb + comb.size() * sizeof(CombineItem);
   std::vector<char> blob(blob_bytes, 0);
   memcpy(blob.data() + o_si, si.data(), batch * sizeof(SampleInfo));
   memcpy(blob.data() + o_tok, tree_tokens, (size_t)N * 4);
   memcpy(blob.data() + o_par, tree_parents, (size_t)N * 4);
   memcpy(blob.data() + o_items, items.data(), items.size() * sizeof(AttnItem));
+  if (!wide.empty()) memcpy(blob.data() + o_wide, wide.data(), wide.size() * sizeof(AttnItem));
   if (!comb.empty()) memcpy(blob.data() + o_comb, comb.data(), comb.size() * sizeof(CombineItem));
   if (int rc = stage_upload(kv, blob.data(), blob_bytes, ws + ly.blob, s)) return rc;
 
@@ -440,6 +450,7 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
   const int32_t* d_tok = (const int32_t*)(ws + ly.blob + o_tok);
   const int32_t* d_par = (const int32_t*)(ws + ly.blob + o_par);
   const AttnItem* d_items = (const AttnItem*)(ws + ly.blob + o_items);
+  const AttnItem* d_wide = (const AttnItem*)(ws + ly.blob + o_wide);
   const CombineItem* d_comb = (const CombineItem*)(ws + ly.blob + o_comb);
   TokInfo* d_toks = (TokInfo*)(ws + ly.toks);
   uint64_t* d_anc = (uint64_t*)(ws + ly.anc);
@@ -478,6 +489,8 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
   aa.anc = d_anc;
   aa.items = d_items;
   aa.n_items = (int)items.size();
+  aa.wide = d_wide;
+  aa.n_wide = (int)wide.size();
   aa.part_o = (float*)(ws + ly.part_o);
   aa.part_ml = (float*)(ws + ly.part_ml);
   aa.out = d_o;

@@ -99,8 +99,10 @@ struct AttnArgs {
   const SampleInfo* samples;
   const TokInfo* toks;
   const uint64_t* anc;      // [N]
-  const AttnItem* items;
+  const AttnItem* items;    // 32-row items (tree_attention_kernel)
   int n_items;
+  const AttnItem* wide;     // 128-row items (tree_attention_wide_kernel)
+  int n_wide;
   float* part_o;            // [slots][32][head_dim]
   float* part_ml;           // [slots][32][2]
   bf16* out;                // [N][n_heads*head_dim]
