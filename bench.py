@@ -36,7 +36,84 @@ def parse():
     p.add_argument("--workload", default="early", choices=["early", "tail", "llama1b"])
     p.add_argument("--cpu-baseline", type=int, default=1, help="0 skips the oracle timing")
     p.add_argument("--seed", type=int, default=None)
+    p.add_argument("--sweep", default=None, metavar="OUT.jsonl",
+                   help="run the strategy-cost sweep (batch x tree budget) and write one JSON "
+                        "line per cell to OUT.jsonl")
     return p.parse_args()
+
+
+def run_sweep(args, out_path):
+    """Strategy-cost surface of the verify step: Llama-3-8B shape, batch in
+    {1,4,16,64,256} x draft-tree budget n in {1,4,8,16,32,64} (top-n nodes by
+    draft logit), one pool of 256 samples with lognormal KV lengths (median
+    2048, sigma 0.8, clipped to [128, 16384]); a batch-B cell uses the first B
+    samples.  Per cell: verify+commit latency, verified and accepted tokens/s
+    and the composite roofline fraction."""
+    import torch
+
+    import paper_2512_04752_amd as sv
+    import workload as wl
+
+    cfg = wl.LLAMA_8B
+    lens_all = [int(x) for x in wl.sweep_lengths()]
+
+    W = wl.make_weights(cfg, 4000, device="cuda")
+    caps = [S + max(wl.SWEEP_BUDGETS) for S in lens_all]
+    max_b = max(wl.SWEEP_BATCHES)
+    ver = sv.Verifier(cfg, W, caps, max_batch=max_b, max_tokens=max_b * max(wl.SWEEP_BUDGETS))
+    gen = torch.Generator(device="cuda").manual_seed(4000)
+    for b, S in enumerate(lens_all):
+        k, v = ver.kv.sample_view(b)
+        wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    rows = []
+    with open(out_path, "w") as f:
+        for B in wl.SWEEP_BATCHES:
+            for n in wl.SWEEP_BUDGETS:
+                w = wl.sweep_workload(B, n)
+                ids, lens = list(range(B)), [int(x) for x in w.seq_lens]
+
+                def greedy_fn(trees):
+                    N = sum(len(t[0]) for t in trees)
+                    dbg = ver.debug_buffers(N, logits=False)
+                    ver.verify(ids, trees, lens, debug=dbg)
+                    g = dbg["argmax"].cpu().tolist()
+                    res, off = [], 0
+                    for t in trees:
+                        res.append(g[off:off + len(t[0])])
+                        off += len(t[0])
+                    return res
+
+                wl.follow_greedy(w.trees, w.branches, w.p_follow, greedy_fn,
+                                 np.random.default_rng(4000 + n))
+                flat = sv.flatten_trees(w.trees)
+                for _ in range(args.warmup):
+                    ver.verify(ids, None, lens, flat=flat, stream=stream)
+                    ver.commit(ids, lens, stream=stream)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(args.steps):
+                    ver.verify(ids, None, lens, flat=flat, stream=stream)
+                    ver.commit(ids, lens, stream=stream)
+                torch.cuda.synchronize()
+                ms = (time.perf_counter() - t0) * 1e3 / args.steps
+                acc = int(ver.accepted_len[:B].sum().item()) + B
+                N = w.n_tokens
+                kv = sum(S + len(t[0]) for S, t in zip(lens, w.trees))
+                t_roof = max(2.0 * N * cfg.gemm_params() / (PEAK_BF16_TFLOPS * 1e12),
+                             2.0 * cfg.gemm_params() / (PEAK_HBM_GBS * 1e9)) + \
+                    kv * cfg.kv_bytes_per_token() / (PEAK_HBM_GBS * 1e9)
+                row = {"batch": B, "budget": n, "tokens": N, "kv_tokens": kv,
+                       "ms_per_step": round(ms, 4), "verified_tokens_per_s": round(N / ms * 1e3, 1),
+                       "accepted_tokens_per_s": round(acc / ms * 1e3, 1),
+                       "accepted_per_sample": round(acc / B, 3),
+                       "t_roof_ms": round(t_roof * 1e3, 4), "roofline_frac": round(t_roof * 1e3 / ms, 4)}
+                rows.append(row)
+                f.write(json.dumps(row) + "\n")
+                f.flush()
+                print(json.dumps(row), file=sys.stderr, flush=True)
+    return rows
 
 
 def describe(name, w):
@@ -63,6 +140,14 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.sweep:
+        rows = run_sweep(args, args.sweep)
+        best = max(rows, key=lambda r: r["accepted_tokens_per_s"])
+        print(json.dumps({"metric": METRIC + " (strategy-cost sweep)", "cells": len(rows),
+                          "best_accepted_tokens_per_s": best["accepted_tokens_per_s"],
+                          "best_cell": {"batch": best["batch"], "budget": best["budget"]},
+                          "out": args.sweep}), flush=True)
+        return
     make = {"early": wl.early_workload, "tail": wl.tail_workload, "llama1b": wl.llama1b_workload}
     w = make[args.workload]() if args.seed is None else make[args.workload](args.seed)
     cfg = w.cfg
