@@ -15,6 +15,7 @@ over a bounded sample of the same workload.
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -33,7 +34,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--workload", default="early", choices=["early", "tail", "llama1b"])
+    p.add_argument("--workload", default="early",
+                   help="early | tail | llama1b | sweep_b<B>_n<n> (one strategy-cost sweep cell)")
     p.add_argument("--cpu-baseline", type=int, default=1, help="0 skips the oracle timing")
     p.add_argument("--seed", type=int, default=None)
     p.add_argument("--sweep", default=None, metavar="OUT.jsonl",
@@ -116,7 +118,21 @@ def run_sweep(args, out_path):
     return rows
 
 
+def make_workload(name, seed):
+    import workload as wl
+    m = re.fullmatch(r"sweep_b(\d+)_n(\d+)", name)
+    if m:
+        return wl.sweep_workload(int(m.group(1)), int(m.group(2)), *(() if seed is None else (seed,)))
+    make = {"early": wl.early_workload, "tail": wl.tail_workload, "llama1b": wl.llama1b_workload}
+    if name not in make:
+        raise SystemExit(f"unknown workload {name!r}")
+    return make[name]() if seed is None else make[name](seed)
+
+
 def describe(name, w):
+    if name.startswith("sweep"):
+        return (f"Llama-3-8B-shape verify, sweep cell: batch {w.batch}, top-{len(w.trees[0][0])} "
+                "draft-logit trees, KV lengths lognormal(median 2048, sigma 0.8) in [128, 16384]")
     if name == "early":
         return ("Llama-3-8B-shape verify, early generation: batch 128, 8-node draft trees "
                 "(4 levels, width <= 3), KV lengths lognormal(median 1024, sigma 0.8) in [128, 8192]")
@@ -148,8 +164,7 @@ def main():
                           "best_cell": {"batch": best["batch"], "budget": best["budget"]},
                           "out": args.sweep}), flush=True)
         return
-    make = {"early": wl.early_workload, "tail": wl.tail_workload, "llama1b": wl.llama1b_workload}
-    w = make[args.workload]() if args.seed is None else make[args.workload](args.seed)
+    w = make_workload(args.workload, args.seed)
     cfg = w.cfg
     plain_trees = [(list(t[0]), list(t[1])) for t in w.trees]   # before greedy steering
 
@@ -192,7 +207,7 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    dominant = {"early": "gemm_gate_up", "llama1b": "gemm_gate_up", "tail": "attention"}[args.workload]
+    dominant = "attention" if args.workload == "tail" else "gemm_gate_up"
     sv.spec_profile_begin(dominant, args.steps * cfg.n_layers + 8)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -221,13 +236,21 @@ def main():
     # Roofline of the dominant kernel: algorithmic work of one launch.
     H, F, d = cfg.hidden, cfg.ffn, cfg.head_dim
     avg_ms = dom_ms / max(dom_launches, 1)
-    if dominant == "gemm_gate_up":
-        work = 2.0 * n_tok * (2 * F) * H                 # flops
-        achieved = work / (avg_ms / 1e3) / 1e12
+    gu_flops = 2.0 * n_tok * (2 * F) * H
+    gu_bytes = 2 * F * H * 2 + n_tok * (H + F) * 2     # weights + activations in + out
+    if dominant == "gemm_gate_up" and gu_flops / (PEAK_BF16_TFLOPS * 1e12) >= \
+            gu_bytes / (PEAK_HBM_GBS * 1e9):
+        achieved = gu_flops / (avg_ms / 1e3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                 "kernel": "gemm_bf16_kernel<EPI_GATE_UP>",
                 "work_per_launch": f"2*{n_tok}*{2 * F}*{H} flop"}
+    elif dominant == "gemm_gate_up":
+        achieved = gu_bytes / (avg_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "kernel": "gemm_bf16_kernel<EPI_GATE_UP> (+ split-K reduce)",
+                "work_per_launch": f"{gu_bytes} bytes (gate and up weights once, rows in and out)"}
     else:
         kv_bytes = sum((int(S) + len(t[0])) for S, t in zip(w.seq_lens, w.trees)) * \
             cfg.n_kv_heads * d * 2 * 2

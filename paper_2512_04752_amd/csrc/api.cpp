@@ -43,7 +43,7 @@ int hip_fail(hipError_t e, const char* what) {
 
 constexpr size_t kAlign = 256;
 constexpr int kPartCap = 8192;          // split-KV partial tiles per call
-constexpr int kTargetItems = 768;       // attention work-groups aimed for (1 per CU at a time)
+constexpr int kTargetSlots = 512;       // attention CU slots aimed for (two rounds of 256 CUs)
 constexpr int kMinChunk = 256;          // keys per split, lower bound
 constexpr int kMaxSplits = 64;          // key ranges per row tile (combine kernel's table)
 
@@ -98,7 +98,7 @@ WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_to
   // attention items: one per row tile and split, then padded per XCD (at most 8x)
   const int64_t items = 8 * (max_row_tiles(c, max_batch, max_tokens) + kPartCap);
   L.blob_bytes = align_up(max_batch * sizeof(SampleInfo)) + 2 * align_up(max_tokens * 4) +
-                 align_up(items * sizeof(AttnItem)) + kAlign +      // narrow + wide lists
+                 align_up(items * sizeof(AttnItem)) + 2 * kAlign +  // narrow + two wide lists
                  align_up(kPartCap * sizeof(CombineItem));
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -345,49 +345,59 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     si[b] = SampleInfo{kv->base[id], kv->cap[id], seq_lens[b], tree_offsets[b],
                        tree_offsets[b + 1] - tree_offsets[b], 0, 0};
   }
-  // Split-KV plan: a row tile is 32 query rows of one (sample, kv head).
-  int64_t key_work = 0, row_tiles = 0;
-  for (int b = 0; b < batch; ++b) {
-    const int64_t tiles = (int64_t)(si[b].ntok * G + 31) / 32;
-    row_tiles += tiles * nkv;
-    key_work += tiles * nkv * (si[b].seq_len + si[b].ntok);
-  }
+  // Split-KV plan.  A row tile is 32 query rows of one (sample, kv head).  A
+  // (sample, kv head) with one tile gets narrow items (4 waves dealing the
+  // keys among themselves, one work-group per CU); 2-4 tiles get one 4-wave
+  // wide group (two per CU); more get 8-wave groups of 8 tiles (one per CU).
+  // Every (sample, kv head) key range is cut into chunks of `chunk` keys,
+  // sized so that the whole call is about kTargetSlots chunk-sized CU
+  // occupancies (a few per CU, for balance), with at most kMaxSplits chunks
+  // per range and at most kPartCap partial states.
+  auto tiles_of = [&](int b) { return (si[b].ntok * G + 31) / 32; };
+  auto keys_of = [&](int b) { return (int64_t)si[b].seq_len + si[b].ntok; };
+  auto cu_weight = [&](int tiles) {       // CU occupancy of one chunk's work-groups
+    return tiles == 1 ? 1.0 : tiles <= 4 ? 0.5 : (double)((tiles + 7) / 8);
+  };
   int64_t max_keys = 0;
-  for (int b = 0; b < batch; ++b) max_keys = std::max<int64_t>(max_keys, si[b].seq_len + si[b].ntok);
-  int64_t chunk = std::max<int64_t>(kMinChunk, (key_work + kTargetItems - 1) / kTargetItems);
-  chunk = std::max<int64_t>(chunk, (max_keys + kMaxSplits - 1) / kMaxSplits);
-  chunk = (chunk + 127) / 128 * 128;
-  auto slots_for = [&](int64_t c) {
+  double work = 0.0;
+  for (int b = 0; b < batch; ++b) {
+    max_keys = std::max(max_keys, keys_of(b));
+    work += (double)nkv * keys_of(b) * cu_weight(tiles_of(b));
+  }
+  auto part_slots = [&](int64_t c) {
     int64_t slots = 0;
     for (int b = 0; b < batch; ++b) {
-      const int64_t ns = (si[b].seq_len + si[b].ntok + c - 1) / c;
-      if (ns > 1) slots += ns * nkv * ((si[b].ntok * G + 31) / 32);
+      const int64_t ns = (keys_of(b) + c - 1) / c;
+      if (ns > 1) slots += ns * nkv * tiles_of(b);
     }
     return slots;
   };
-  while (slots_for(chunk) > kPartCap) chunk *= 2;
-  // Work items.  A (sample, kv head) with at most 32 query rows gets narrow
-  // items (one 32-row tile); more rows get wide items of 128 rows (4 tiles),
-  // which read each key range once for all their rows.  Split key ranges
-  // write their partial states to per-tile slots part + tile * ns + split.
-  std::vector<AttnItem> items, wide;
+  auto round128 = [](int64_t x) { return (x + 127) / 128 * 128; };
+  int64_t chunk = round128(std::max<int64_t>(
+      {(int64_t)kMinChunk, (max_keys + kMaxSplits - 1) / kMaxSplits, (int64_t)(work / kTargetSlots)}));
+  while (part_slots(chunk) > kPartCap) chunk += 128;    // terminates: one chunk per range has none
+  // Work items.  Split key ranges write their partial states to per-tile
+  // slots part + tile * ns + split.
+  std::vector<AttnItem> items, wide4, wide8;
   std::vector<CombineItem> comb;
-  items.reserve(row_tiles * 2);
   int part = 0;
   for (int b = 0; b < batch; ++b) {
-    const int keys = si[b].seq_len + si[b].ntok;
+    const int keys = (int)keys_of(b);
     const int ns = (int)((keys + chunk - 1) / chunk);
-    const int tiles = (si[b].ntok * G + 31) / 32;
+    const int tiles = tiles_of(b);
     for (int g = 0; g < nkv; ++g) {
       for (int t = 0; t < tiles && ns > 1; ++t)
         comb.push_back(CombineItem{b, g, t * 32, ns, part + t * ns, 0, 0, 0});
       for (int k = 0; k < ns; ++k) {
         const int k0 = (int)(k * chunk), k1 = (int)std::min<int64_t>(keys, (k + 1) * chunk);
+        const int p = ns > 1 ? part + k : 0;
         if (tiles == 1)
-          items.push_back(AttnItem{b, g, 0, k0, k1, ns, ns > 1 ? part + k : 0, 0});
+          items.push_back(AttnItem{b, g, 0, k0, k1, ns, p, 0});
+        else if (tiles <= 4)
+          wide4.push_back(AttnItem{b, g, 0, k0, k1, ns, p, 0});
         else
-          for (int rg = 0; rg < (tiles + 3) / 4; ++rg)
-            wide.push_back(AttnItem{b, g, rg * 128, k0, k1, ns, ns > 1 ? part + rg * 4 * ns + k : 0, 0});
+          for (int rg = 0; rg < (tiles + 7) / 8; ++rg)
+            wide8.push_back(AttnItem{b, g, rg * 256, k0, k1, ns, ns > 1 ? p + rg * 8 * ns : 0, 0});
       }
       if (ns > 1) part += ns * tiles;
     }
@@ -427,22 +437,25 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     list.swap(dealt);
   };
   deal(items);
-  deal(wide);
+  deal(wide4);
+  deal(wide8);
 
   // ---- one upload of the per-call descriptors ----
   const size_t o_si = 0;
   const size_t o_tok = align_up(batch * sizeof(SampleInfo));
   const size_t o_par = o_tok + align_up((size_t)N * 4);
   const size_t o_items = o_par + align_up((size_t)N * 4);
-  const size_t o_wide = o_items + align_up(items.size() * sizeof(AttnItem));
-  const size_t o_comb = o_wide + align_up(wide.size() * sizeof(AttnItem));
+  const size_t o_wide4 = o_items + align_up(items.size() * sizeof(AttnItem));
+  const size_t o_wide8 = o_wide4 + align_up(wide4.size() * sizeof(AttnItem));
+  const size_t o_comb = o_wide8 + align_up(wide8.size() * sizeof(AttnItem));
   const size_t blob_bytes = o_comb + comb.size() * sizeof(CombineItem);
   std::vector<char> blob(blob_bytes, 0);
   memcpy(blob.data() + o_si, si.data(), batch * sizeof(SampleInfo));
   memcpy(blob.data() + o_tok, tree_tokens, (size_t)N * 4);
   memcpy(blob.data() + o_par, tree_parents, (size_t)N * 4);
   memcpy(blob.data() + o_items, items.data(), items.size() * sizeof(AttnItem));
-  if (!wide.empty()) memcpy(blob.data() + o_wide, wide.data(), wide.size() * sizeof(AttnItem));
+  if (!wide4.empty()) memcpy(blob.data() + o_wide4, wide4.data(), wide4.size() * sizeof(AttnItem));
+  if (!wide8.empty()) memcpy(blob.data() + o_wide8, wide8.data(), wide8.size() * sizeof(AttnItem));
   if (!comb.empty()) memcpy(blob.data() + o_comb, comb.data(), comb.size() * sizeof(CombineItem));
   if (int rc = stage_upload(kv, blob.data(), blob_bytes, ws + ly.blob, s)) return rc;
 
@@ -450,7 +463,8 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
   const int32_t* d_tok = (const int32_t*)(ws + ly.blob + o_tok);
   const int32_t* d_par = (const int32_t*)(ws + ly.blob + o_par);
   const AttnItem* d_items = (const AttnItem*)(ws + ly.blob + o_items);
-  const AttnItem* d_wide = (const AttnItem*)(ws + ly.blob + o_wide);
+  const AttnItem* d_wide4 = (const AttnItem*)(ws + ly.blob + o_wide4);
+  const AttnItem* d_wide8 = (const AttnItem*)(ws + ly.blob + o_wide8);
   const CombineItem* d_comb = (const CombineItem*)(ws + ly.blob + o_comb);
   TokInfo* d_toks = (TokInfo*)(ws + ly.toks);
   uint64_t* d_anc = (uint64_t*)(ws + ly.anc);
@@ -489,8 +503,10 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
   aa.anc = d_anc;
   aa.items = d_items;
   aa.n_items = (int)items.size();
-  aa.wide = d_wide;
-  aa.n_wide = (int)wide.size();
+  aa.wide = d_wide4;
+  aa.n_wide = (int)wide4.size();
+  aa.wide8 = d_wide8;
+  aa.n_wide8 = (int)wide8.size();
   aa.part_o = (float*)(ws + ly.part_o);
   aa.part_ml = (float*)(ws + ly.part_ml);
   aa.out = d_o;

@@ -5,7 +5,7 @@
 // sees every committed key [0, S_b) and, of the tree keys at cache slots
 // S_b + t, exactly its ancestors t (itself included), given as a bitmask.
 //
-// Both kernels process 32-key blocks per wave with the transposed products
+// Every kernel processes 32-key blocks per wave with the transposed products
 //
 //   S^T (32 keys x 32 rows) = K . Q^T   v_mfma_f32_32x32x16_bf16, A = K (LDS)
 //   online softmax per row              each lane owns one row (16 of its keys,
@@ -20,15 +20,22 @@
 // and the transposing V reads (4 rows x 4 columns of 8 bytes) are free of
 // bank conflicts.
 //
+// The softmax runs in the base-2 domain (scores scaled by log2(e)/sqrt(d)
+// inside one FMA, v_exp_f32 directly).  The running output is rescaled only
+// when some row's maximum grew in this block (a wave-uniform test); with a
+// long prefix the maximum settles early and most blocks skip the rescale.
+//
 //   * tree_attention_kernel: one 32-row tile per work-group (at most 32 query
 //     rows per KV head, e.g. 8-node trees with 4 query heads per KV head).  The
 //     key range is dealt to the 4 waves in 32-key blocks; each wave streams
 //     its blocks through a private LDS ring (no work-group barrier), and the
 //     four partial softmax states are merged through LDS at the end.
-//   * tree_attention_wide_kernel: 128 query rows per work-group (larger
-//     trees).  Wave w owns rows 32w..32w+31; all four waves share 64-key K/V
-//     stages loaded cooperatively, so the range is read once per 128 rows, and
-//     each wave ends with complete rows (no merge).
+//   * tree_attention_wide_kernel<HD, NW>: 32*NW query rows per work-group
+//     (NW = 4 or 8 waves; larger trees).  Wave w owns rows 32w..32w+31; all
+//     waves share a ring of 64-key K/V stages loaded cooperatively, so the
+//     key range is read once per 32*NW rows, and each wave ends with complete
+//     rows (no merge).  Both score blocks of a stage are computed before the
+//     first softmax, so the second block's MFMAs overlap the first softmax.
 //
 // Long key ranges are split into ranges processed in parallel and merged by
 // attention_combine_kernel.
@@ -58,13 +65,78 @@ __device__ __forceinline__ int kswz(int key) {
 // V rows: the transposing read touches 4 consecutive rows x 32 bytes.
 __device__ __forceinline__ int vswz(int key) { return (key & 3) << 1; }
 
+// Wait until at most N vector-memory operations of this wave are in flight.
 template <int N>
 __device__ __forceinline__ void wait_vm() {
-  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-  else if constexpr (N == 24) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
-  else static_assert(N < 0, "unsupported vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// max / sum of a value and its copy in lane ^ 32 (v_permlane32_swap: each
+// lane ends with both halves' values in the two results).
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Scores of keys this lane's row may not see become -inf.
+__device__ __forceinline__ void mask_block(f32x16& s, int kb, int key1, int seq_len, uint64_t anc,
+                                           int h) {
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int key = kb + 8 * (e >> 2) + 4 * h + (e & 3);
+    const int tt = key - seq_len;
+    const bool anc_bit = (anc >> (tt & 63)) & 1ull;
+    const bool vis = (key < key1) & ((tt < 0) | anc_bit);
+    s[e] = vis ? s[e] : -INFINITY;
+  }
+}
+
+// Online-softmax update of one 64-key stage: raw scores sa (keys kb..kb+31)
+// and sb (kb+32..kb+63), one running-maximum update and at most one rescale
+// of the output for both.
+template <int NB>
+__device__ __forceinline__ void softmax_stage(bool mask_a, bool mask_b, f32x16& sa, f32x16& sb, int kb,
+                                              int key1, int seq_len, uint64_t anc, int h, float sl2,
+                                              float& m_run, float& l_run, f32x16 (&o)[NB],
+                                              bf16x8 (&pa)[2], bf16x8 (&pb)[2]) {
+  if (mask_a) mask_block(sa, kb, key1, seq_len, anc, h);
+  if (mask_b) mask_block(sb, kb + 32, key1, seq_len, anc, h);
+  float smax = fmaxf(sa[0], sb[0]);
+#pragma unroll
+  for (int e = 1; e < 16; ++e) smax = fmaxf(smax, fmaxf(sa[e], sb[e]));
+  smax = max_xor32(smax);
+  const float m_new = fmaxf(m_run, smax * sl2);
+  if (__ballot(m_new > m_run)) {
+    const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) o[i] *= alpha;
+    m_run = m_new;
+  }
+  const float mb = m_run == -INFINITY ? 0.f : m_run;
+  float psum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const float p0 = fast_exp2(fmaf(sa[e], sl2, -mb));
+    const float p1 = fast_exp2(fmaf(sb[e], sl2, -mb));
+    psum += p0 + p1;
+    pa[e >> 3][e & 7] = (bf16)p0;
+    pb[e >> 3][e & 7] = (bf16)p1;
+  }
+  l_run += psum;
+}
+
+// K fragment (A operand of S^T = K.Q^T) of k-step ks for key row `row` of a
+// swizzled K block: 8 consecutive dims 16 ks + 8 h.
+template <int HD>
+__device__ __forceinline__ bf16x8 k_fragment(const char* k0, int row, int ks, int h) {
+  return *(const bf16x8*)(k0 + row * (HD * 2) + (((2 * ks + h) ^ kswz<HD>(row)) << 4));
 }
 
 // V^T fragment (A operand) of k-step kst for output dims [32i, 32i+32) from
@@ -88,44 +160,102 @@ __device__ __forceinline__ bf16x8 vt_fragment(const char* v0, int kst, int i, in
   return f;
 }
 
-// Online-softmax update of one 32-key block: masks, rescales o, returns P^T.
-template <int NB>
+// Online-softmax update of one 32-key block.  s holds the raw scores K.q of
+// keys kb + 8(e/4) + 4h + e%4 of this lane's row; m_run is the running
+// maximum of the scaled scores (base-2 domain).  Produces P^T in bf16 and
+// accumulates the row sum of the unrounded probabilities.
+template <bool MASK, int NB>
 __device__ __forceinline__ void softmax_block(f32x16& s, int kb, int key1, int seq_len, uint64_t anc,
                                               int h, float sl2, float& m_run, float& l_run,
                                               f32x16 (&o)[NB], bf16x8 (&pb)[2]) {
-  float smax = -INFINITY;
-  if (kb + KBLK <= seq_len && kb + KBLK <= key1) {       // wholly committed prefix: no mask
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      s[e] *= sl2;
-      smax = fmaxf(smax, s[e]);
-    }
-  } else {
+  if constexpr (MASK) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int key = kb + 8 * (e >> 2) + 4 * h + (e & 3);
       const int tt = key - seq_len;
       const bool anc_bit = (anc >> (tt & 63)) & 1ull;
       const bool vis = (key < key1) & ((tt < 0) | anc_bit);
-      s[e] = vis ? s[e] * sl2 : -INFINITY;
-      smax = fmaxf(smax, s[e]);
+      s[e] = vis ? s[e] : -INFINITY;
     }
   }
+  float smax = s[0];
+#pragma unroll
+  for (int e = 1; e < 16; ++e) smax = fmaxf(smax, s[e]);
   smax = fmaxf(smax, __shfl_xor(smax, 32));
-  const float m_new = fmaxf(m_run, smax);
-  const bool none = (m_new == -INFINITY);
-  const float alpha = none ? 1.f : exp2f(m_run - m_new);
+  const float m_new = fmaxf(m_run, smax * sl2);
+  if (__ballot(m_new > m_run)) {
+    // exp2(m_run - m_new) is 0 for a first visible block (m_run = -inf) and
+    // 1 for rows whose maximum did not move; rows with nothing visible yet
+    // keep alpha = 1.
+    const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) o[i] *= alpha;
+    m_run = m_new;
+  }
+  const float mb = m_run == -INFINITY ? 0.f : m_run;
   float psum = 0.f;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
-    const float pe = none ? 0.f : exp2f(s[e] - m_new);
+    const float pe = fast_exp2(fmaf(s[e], sl2, -mb));     // masked: exp2(-inf) = 0
     psum += pe;
     pb[e >> 3][e & 7] = (bf16)pe;
   }
-  l_run = l_run * alpha + psum;
-  m_run = m_new;
+  l_run += psum;
+}
+
+template <int NB>
+__device__ __forceinline__ void softmax_any(bool mask, f32x16& s, int kb, int key1, int seq_len,
+                                            uint64_t anc, int h, float sl2, float& m_run,
+                                            float& l_run, f32x16 (&o)[NB], bf16x8 (&pb)[2]) {
+  if (mask) softmax_block<true, NB>(s, kb, key1, seq_len, anc, h, sl2, m_run, l_run, o, pb);
+  else softmax_block<false, NB>(s, kb, key1, seq_len, anc, h, sl2, m_run, l_run, o, pb);
+}
+
+// O^T += V^T . P^T for one 32-key block whose V rows start at v0.
+template <int HD>
+__device__ __forceinline__ void pv_block(const char* v0, const bf16x8 (&pb)[2], f32x16 (&o)[HD / 32],
+                                         int lane) {
 #pragma unroll
-  for (int i = 0; i < NB; ++i) o[i] *= alpha;
+  for (int kst = 0; kst < 2; ++kst)
+#pragma unroll
+    for (int i = 0; i < HD / 32; ++i)
+      o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt_fragment<HD>(v0, kst, i, lane), pb[kst], o[i],
+                                                    0, 0, 0);
+}
+
+// Write a lane's finished row: dims 32i + 8q + 4h + {0..3} sit in
+// o[i][4q..4q+3].  nsplit == 1: normalised bf16 output; otherwise the
+// unnormalised fp32 partial and (m, l) of split slot `slot`.
+template <int HD>
+__device__ __forceinline__ void store_row(const AttnArgs& a, const f32x16 (&o)[HD / 32], float m_run,
+                                          float l_run, int nsplit, int slot, int r, int h,
+                                          size_t out_row, int head) {
+  if (nsplit == 1) {
+    const float inv = 1.f / l_run;
+    bf16* dst = a.out + out_row * (size_t)a.n_heads * HD + head * HD + 4 * h;
+#pragma unroll
+    for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        bf16x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[i][4 * q + j] * inv);
+        *(bf16x4*)(dst + 32 * i + 8 * q) = v;
+      }
+  } else {
+    float* dst = a.part_o + ((size_t)slot * 32 + r) * HD + 4 * h;
+#pragma unroll
+    for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *(f32x4*)(dst + 32 * i + 8 * q) =
+            f32x4{o[i][4 * q], o[i][4 * q + 1], o[i][4 * q + 2], o[i][4 * q + 3]};
+    if (h == 0) {
+      a.part_ml[((size_t)slot * 32 + r) * 2] = m_run;
+      a.part_ml[((size_t)slot * 32 + r) * 2 + 1] = l_run;
+    }
+  }
 }
 
 template <int HD>
@@ -141,13 +271,18 @@ struct AttnCfg {
   static constexpr int O_STRIDE = HD + 1;               // floats per merge row
   static constexpr int MERGE_BYTES = 4 * 32 * O_STRIDE * 4 + 4 * 32 * 2 * 4;
   static constexpr int SMEM = (4 * WAVE_RING) > MERGE_BYTES ? (4 * WAVE_RING) : MERGE_BYTES;
-  // wide kernel: shared 2-stage ring of 64-key stages
+  // wide kernels: shared ring of 64-key stages
   static constexpr int WKEYS = 64;
   static constexpr int W_KV = WKEYS * ROW;              // K (or V) bytes per stage
   static constexpr int W_STAGE = 2 * W_KV;
-  static constexpr int W_SMEM = 2 * W_STAGE;
-  static constexpr int W_LOADS = W_KV / 1024 / 4;       // per wave, for K (and for V)
 };
+
+// Wide-kernel ring depth: 8-wave groups own a CU (two waves per SIMD) and
+// take four stages; 4-wave groups run two per CU within 160 KB of LDS.
+template <int HD, int NW>
+constexpr int wide_stages() {
+  return (NW == 8 || HD == 64) ? 4 : 2;
+}
 
 template <int HD>
 __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
@@ -191,6 +326,7 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
   // Blocks of this wave: w, w+4, w+8, ... of the item's range.
   const int nblk = (it.key1 - it.key0 + KBLK - 1) / KBLK;
   const int mine = nblk > w ? (nblk - w + 3) / 4 : 0;
+  const int mask_from = min(si.seq_len, it.key1);   // blocks ending past this need the mask
 
   // Lane l of wave-load j copies row (j*ROWS_PER_LOAD + l / DC) of the block
   // into physical chunk l % DC; keys past the range repeat the last key,
@@ -235,22 +371,15 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
     f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < HD / 16; ks += 2) {
-      const bf16x8 k0 = *(const bf16x8*)(st + r * C::ROW + (((2 * ks + h) ^ kswz<HD>(r)) << 4));
-      const bf16x8 k1 = *(const bf16x8*)(st + r * C::ROW + (((2 * ks + 2 + h) ^ kswz<HD>(r)) << 4));
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks + 1], s1, 0, 0, 0);
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_fragment<HD>(st, r, ks, h), qf[ks], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_fragment<HD>(st, r, ks + 1, h), qf[ks + 1], s1, 0,
+                                                   0, 0);
     }
     f32x16 s = s0 + s1;
     bf16x8 pb[2];
-    softmax_block<NB>(s, kb, it.key1, si.seq_len, anc_row, h, sl2, m_run, l_run, o, pb);
-
-    // O^T += V^T . P^T
-#pragma unroll
-    for (int kst = 0; kst < 2; ++kst)
-#pragma unroll
-      for (int i = 0; i < NB; ++i)
-        o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt_fragment<HD>(st + C::KV_BYTES, kst, i, lane),
-                                                      pb[kst], o[i], 0, 0, 0);
+    softmax_any<NB>(kb + KBLK > mask_from, s, kb, it.key1, si.seq_len, anc_row, h, sl2, m_run, l_run,
+                    o, pb);
+    pv_block<HD>(st + C::KV_BYTES, pb, o, lane);
   }
   l_run += __shfl_xor(l_run, 32);
 
@@ -283,7 +412,7 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
     for (int ww = 0; ww < 4; ++ww) {
       const float mw = ml_sh[(ww * 32 + row) * 2];
-      const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
+      const float f = (mw == -INFINITY) ? 0.f : fast_exp2(mw - M);
       O += f * o_sh[(ww * 32 + row) * C::O_STRIDE + d];
       L += f * ml_sh[(ww * 32 + row) * 2 + 1];
     }
@@ -299,21 +428,28 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
   }
 }
 
-// 128 query rows per work-group: wave w owns rows it.row0 + 32w .. +31 and
-// all keys of the range, streamed in shared 64-key stages (two-stage ring,
-// one barrier per stage).  With the range split, wave w's partial state goes
-// to slot it.part + w * it.nsplit (its row tile's slot for this split).
-template <int HD>
-__global__ __launch_bounds__(NT, 2) void tree_attention_wide_kernel(AttnArgs a) {
+// 32*NW query rows per work-group: wave w owns rows it.row0 + 32w .. +31 and
+// all keys of the range, streamed in shared 64-key stages through an NS-deep
+// ring (one barrier per stage, NS-2 stages in flight behind the one being
+// read).  With the range split, wave w's partial state goes to slot
+// it.part + w * it.nsplit (its row tile's slot for this split).
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void tree_attention_wide_kernel(AttnArgs a,
+                                                                       const AttnItem* items,
+                                                                       int n_items) {
   using C = AttnCfg<HD>;
   constexpr int DC = HD / 8;
   constexpr int NB = HD / 32;
+  constexpr int NS = wide_stages<HD, NW>();
+  constexpr int W_LOADS = C::W_KV / 1024 / NW;   // per wave and stage, for K (and for V)
+  constexpr int LPW = 2 * W_LOADS;                // vector-memory ops per wave and stage
+  static_assert(W_LOADS >= 1, "stage too small for the work-group");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int per_xcd = gridDim.x >> 3;
   const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (item >= a.n_wide) return;
-  const AttnItem it = a.wide[item];
+  if (item >= n_items) return;
+  const AttnItem it = items[item];
   if (it.sample < 0) return;
   const SampleInfo si = a.samples[it.sample];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -338,20 +474,22 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_wide_kernel(AttnArgs a) 
   const bf16* vbase = kbase + (size_t)a.n_kv_heads * head_stride;
 
   const int nstage = (it.key1 - it.key0 + C::WKEYS - 1) / C::WKEYS;
-  // Wave w loads rows [16w, 16w+16) of each stage's K and V.
+  const int mask_from = min(si.seq_len, it.key1);
+  // Wave w loads rows [W_LOADS*ROWS_PER_LOAD*w, +W_LOADS*ROWS_PER_LOAD) of
+  // each stage's K and V.
   const int lrow = lane / DC, lch = lane % DC;
   auto issue = [&](int t, int slot) {
     const int kb = it.key0 + t * C::WKEYS;
     char* st = smem + slot * C::W_STAGE;
 #pragma unroll
-    for (int j = 0; j < C::W_LOADS; ++j) {
-      const int row = (w * C::W_LOADS + j) * C::ROWS_PER_LOAD + lrow;
+    for (int j = 0; j < W_LOADS; ++j) {
+      const int row = (w * W_LOADS + j) * C::ROWS_PER_LOAD + lrow;
       int key = kb + row;
       key = key < it.key1 ? key : it.key1 - 1;
       load_lds16(kbase + (size_t)key * HD + ((lch ^ kswz<HD>(row)) << 3),
-                 st + (w * C::W_LOADS + j) * 1024);
+                 st + (w * W_LOADS + j) * 1024);
       load_lds16(vbase + (size_t)key * HD + ((lch ^ vswz(row)) << 3),
-                 st + C::W_KV + (w * C::W_LOADS + j) * 1024);
+                 st + C::W_KV + (w * W_LOADS + j) * 1024);
     }
   };
 
@@ -361,56 +499,59 @@ __global__ __launch_bounds__(NT, 2) void tree_attention_wide_kernel(AttnArgs a) 
 #pragma unroll
   for (int i = 0; i < NB; ++i) o[i] = f32x16{};
 
-  if (nstage > 0) issue(0, 0);
-  for (int t = 0; t < nstage; ++t) {
-    wait_vm<0>();
-    __syncthreads();      // stage t visible to all waves; stage t-1 fully consumed
-    if (t + 1 < nstage) issue(t + 1, (t + 1) & 1);
-    const char* st = smem + (t & 1) * C::W_STAGE;
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const char* kblk = st + half * KBLK * C::ROW;
-      const int kb = it.key0 + t * C::WKEYS + half * KBLK;
-      f32x16 s0 = f32x16{}, s1 = f32x16{};
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < nstage) issue(t, t);
+  // Unrolled by the ring depth so that every LDS address is a per-lane base
+  // plus an immediate.
+  for (int t0 = 0; t0 < nstage; t0 += NS) {
 #pragma unroll
-      for (int ks = 0; ks < HD / 16; ks += 2) {
-        const int krow = half * KBLK + r;
-        const bf16x8 k0 = *(const bf16x8*)(kblk + r * C::ROW + (((2 * ks + h) ^ kswz<HD>(krow)) << 4));
-        const bf16x8 k1 = *(const bf16x8*)(kblk + r * C::ROW + (((2 * ks + 2 + h) ^ kswz<HD>(krow)) << 4));
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks + 1], s1, 0, 0, 0);
+    for (int u = 0; u < NS; ++u) {
+      const int t = t0 + u;
+      if (t >= nstage) break;
+      // Stage t must have landed; stages t+1 .. t+NS-2 may stay in flight.
+      const int pending = min(NS - 2, nstage - 1 - t);
+      if constexpr (NS == 4) {
+        if (pending >= 2) wait_vm<2 * LPW>();
+        else if (pending == 1) wait_vm<LPW>();
+        else wait_vm<0>();
+      } else {
+        wait_vm<0>();
       }
-      f32x16 s = s0 + s1;
-      bf16x8 pb[2];
-      softmax_block<NB>(s, kb, it.key1, si.seq_len, anc_row, h, sl2, m_run, l_run, o, pb);
-      const char* vblk = st + C::W_KV + half * KBLK * C::ROW;
-#pragma unroll
-      for (int kst = 0; kst < 2; ++kst)
-#pragma unroll
-        for (int i = 0; i < NB; ++i)
-          o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt_fragment<HD>(vblk, kst, i, lane), pb[kst],
-                                                        o[i], 0, 0, 0);
-    }
-  }
-  l_run += __shfl_xor(l_run, 32);
+      __syncthreads();    // stage t visible to all waves; stage t-1 fully consumed
+      if (t + NS - 1 < nstage) issue(t + NS - 1, (u + NS - 1) % NS);
+      const char* st = smem + u * C::W_STAGE;
+      const int kb = it.key0 + t * C::WKEYS;
 
-  // Lane (r, h) holds dims 32i + 8(e/4) + 4h + e%4 of row r.
-  if (!row_ok) return;
-  const int slot = it.part + w * it.nsplit;
+      // Scores of both 32-key blocks (two independent MFMA chains), K
+      // fragments read one k-step ahead.
+      f32x16 sa = f32x16{}, sb = f32x16{};
+      bf16x8 ka = k_fragment<HD>(st, r, 0, h), kb2 = k_fragment<HD>(st, KBLK + r, 0, h);
 #pragma unroll
-  for (int i = 0; i < NB; ++i)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int d = i * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-      if (it.nsplit == 1)
-        a.out[(size_t)(si.tok0 + node) * nq_hd + head * HD + d] = (bf16)(o[i][e] / l_run);
-      else
-        a.part_o[((size_t)slot * 32 + r) * HD + d] = o[i][e];
+      for (int ks = 0; ks < HD / 16; ++ks) {
+        bf16x8 na, nb;
+        if (ks + 1 < HD / 16) {
+          na = k_fragment<HD>(st, r, ks + 1, h);
+          nb = k_fragment<HD>(st, KBLK + r, ks + 1, h);
+        }
+        sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], sa, 0, 0, 0);
+        sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb2, qf[ks], sb, 0, 0, 0);
+        if (ks + 1 < HD / 16) {
+          ka = na;
+          kb2 = nb;
+        }
+      }
+      bf16x8 pa[2], pb[2];
+      softmax_stage<NB>(kb + KBLK > mask_from, kb + 2 * KBLK > mask_from, sa, sb, kb, it.key1,
+                        si.seq_len, anc_row, h, sl2, m_run, l_run, o, pa, pb);
+      pv_block<HD>(st + C::W_KV, pa, o, lane);
+      pv_block<HD>(st + C::W_KV + KBLK * C::ROW, pb, o, lane);
     }
-  if (it.nsplit > 1 && h == 0) {
-    a.part_ml[((size_t)slot * 32 + r) * 2] = m_run;
-    a.part_ml[((size_t)slot * 32 + r) * 2 + 1] = l_run;
   }
+  l_run = sum_xor32(l_run);
+
+  if (!row_ok) return;
+  store_row<HD>(a, o, m_run, l_run, it.nsplit, it.part + w * it.nsplit, r, h, si.tok0 + node, head);
 }
 
 // Merge the partial states of a row tile's key ranges: one block per query
@@ -439,7 +580,7 @@ __global__ __launch_bounds__(HD) void attention_combine_kernel(AttnArgs a) {
     for (int sp = d; sp < ci.nsplit; sp += 64) {
       const size_t slot = (size_t)(ci.part0 + sp) * 32 + row;
       const float ms = a.part_ml[slot * 2];
-      const float f = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
+      const float f = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M);
       if (sp < MAXS) wgt[sp] = f;
       L += f * a.part_ml[slot * 2 + 1];
     }
@@ -454,21 +595,36 @@ __global__ __launch_bounds__(HD) void attention_combine_kernel(AttnArgs a) {
   a.out[(size_t)(si.tok0 + nd) * a.n_heads * HD + hq * HD + d] = (bf16)(O * inv_l);
 }
 
+template <int HD, int NW>
+hipError_t launch_wide(const AttnArgs& a, const AttnItem* items, int n, hipStream_t s) {
+  using C = AttnCfg<HD>;
+  constexpr int SMEM = wide_stages<HD, NW>() * C::W_STAGE;
+  static bool configured = false;
+  if (!configured) {
+    const hipError_t e = hipFuncSetAttribute((const void*)tree_attention_wide_kernel<HD, NW>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  tree_attention_wide_kernel<HD, NW><<<(n + 7) / 8 * 8, 64 * NW, SMEM, s>>>(a, items, n);
+  return hipSuccess;
+}
+
 template <int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   using C = AttnCfg<HD>;
   static bool configured = false;
   if (!configured) {
-    hipError_t e = hipFuncSetAttribute((const void*)tree_attention_kernel<HD>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::SMEM);
-    if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute((const void*)tree_attention_wide_kernel<HD>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, C::W_SMEM);
+    const hipError_t e = hipFuncSetAttribute((const void*)tree_attention_kernel<HD>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, C::SMEM);
     if (e != hipSuccess) return e;
     configured = true;
   }
+  hipError_t e = hipSuccess;
   if (a.n_items) tree_attention_kernel<HD><<<(a.n_items + 7) / 8 * 8, NT, C::SMEM, s>>>(a);
-  if (a.n_wide) tree_attention_wide_kernel<HD><<<(a.n_wide + 7) / 8 * 8, NT, C::W_SMEM, s>>>(a);
+  if (a.n_wide && e == hipSuccess) e = launch_wide<HD, 4>(a, a.wide, a.n_wide, s);
+  if (a.n_wide8 && e == hipSuccess) e = launch_wide<HD, 8>(a, a.wide8, a.n_wide8, s);
+  if (e != hipSuccess) return e;
   if (a.n_comb) attention_combine_kernel<HD><<<dim3(a.n_comb, 32), HD, 0, s>>>(a);
   return hipGetLastError();
 }
@@ -476,7 +632,7 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
-  if (a.n_items == 0 && a.n_wide == 0) return hipSuccess;
+  if (a.n_items == 0 && a.n_wide == 0 && a.n_wide8 == 0) return hipSuccess;
   if (a.head_dim == 128) return launch_hd<128>(a, s);
   if (a.head_dim == 64) return launch_hd<64>(a, s);
   return hipErrorInvalidValue;

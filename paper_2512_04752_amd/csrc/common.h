@@ -101,8 +101,10 @@ struct AttnArgs {
   const uint64_t* anc;      // [N]
   const AttnItem* items;    // 32-row items (tree_attention_kernel)
   int n_items;
-  const AttnItem* wide;     // 128-row items (tree_attention_wide_kernel)
+  const AttnItem* wide;     // 128-row items (tree_attention_wide_kernel<HD, 4>)
   int n_wide;
+  const AttnItem* wide8;    // 256-row items (tree_attention_wide_kernel<HD, 8>)
+  int n_wide8;
   float* part_o;            // [slots][32][head_dim]
   float* part_ml;           // [slots][32][2]
   bf16* out;                // [N][n_heads*head_dim]

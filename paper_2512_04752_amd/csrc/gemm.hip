@@ -11,9 +11,9 @@
 //   EPI_ARGMAX   LM head: per row, the (max, lowest index) over each wave's
 //                column slab, optionally also the fp32 logits
 //
-// Structure (one 256-thread work-group = 4 waves in a 2 x 2 grid, output tile
-// BM x BN, each wave BM/2 x BN/2 built from 32 x 32 v_mfma_f32_32x32x16_bf16
-// blocks; K step 64):
+// Structure (one 256-thread work-group = 4 waves in a WM x WN grid, output
+// tile BM x BN, each wave BM/WM x BN/WN built from 32 x 32
+// v_mfma_f32_32x32x16_bf16 blocks; K step 64):
 //   * operand tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 (no
 //     register staging) into a two-stage ring; the next K step is in flight
 //     while the current one is multiplied, and one barrier per K step both
@@ -23,14 +23,15 @@
 //     reads (16 consecutive rows, one chunk) hit all 64 LDS banks once;
 //   * fragments of the next 16-wide k-step are read from LDS into a second
 //     register set while the current set feeds the MFMAs.
-// Work-groups are dealt round-robin over the 8 XCDs; the tile order is
-// remapped so that the M tiles sharing one weight tile run on one XCD and hit
-// its L2 instead of HBM.
+// Tile shapes: 256 x 256 (4 waves of 128 x 128) when the product has enough
+// tiles for the 256 CUs, 128 x 128 otherwise, and 32 x 256 / 64 x 256 for few
+// rows, where the weights are streamed and the rows are few.  Work-groups are
+// dealt round-robin over the 8 XCDs; the tile order is remapped so that the M
+// tiles sharing one weight tile run on one XCD and hit its L2.
 //
-// Products with too few output tiles to fill the 256 CUs (few rows, narrow
-// outputs) split K: each split writes its fp32 tile to a partial buffer and a
-// second kernel sums the splits in a fixed order (bitwise reproducible) and
-// applies the same epilogue.
+// Products with too few output tiles to fill the CUs split K: each split
+// writes its fp32 tile to a partial buffer and a second kernel sums the splits
+// in a fixed order (bitwise reproducible) and applies the same epilogue.
 #include <algorithm>
 
 #include "common.h"
@@ -50,14 +51,14 @@ __device__ __forceinline__ void load_lds16(const void* g, void* lds) {
 
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
-// Virtual-column mapping.  Column u of an output tile belongs to wave
+// Virtual-column mapping.  Column u of an output tile belongs to wave column
 // wn = u / TN, MFMA block nb = (u % TN) / 32, lane column c = u % 32.  For
-// EPI_QKV and EPI_GATE_UP, blocks (2p, 2p+1) of a wave form pair P = wn*NB/2+p
-// of the tile: rotary partners (dims j, j + d/2) or (gate, up) of one feature.
+// EPI_QKV and EPI_GATE_UP, blocks (2p, 2p+1) of a wave column form pair
+// P = (u % BN) / 64 of the tile: rotary partners (dims j, j + d/2) or
+// (gate, up) of one feature.
 template <int EPI, int BN>
 __device__ __forceinline__ const bf16* weight_row(const GemmArgs& a, int tn, int u) {
-  constexpr int TN = BN / 2, NB = TN / 32;
-  const int wn = u / TN, nb = (u % TN) >> 5, c = u & 31;
+  const int P = u >> 6, blk = (u >> 5) & 1, c = u & 31;
   if constexpr (EPI == EPI_QKV) {
     const int vs = tn * BN;
     const bf16* base;
@@ -66,13 +67,11 @@ __device__ __forceinline__ const bf16* weight_row(const GemmArgs& a, int tn, int
     else if (vs < a.n0 + a.n1) { base = a.B1; local = vs - a.n0; }
     else { base = a.B2; local = vs - a.n0 - a.n1; }
     const int hd = a.head_dim, qpd = hd / 64;
-    const int P = wn * (NB / 2) + (nb >> 1), blk = nb & 1;
     const int head = P / qpd, dim = (P % qpd) * 32 + blk * (hd / 2) + c;
     return base + (size_t)(local + head * hd + dim) * a.K;
   } else if constexpr (EPI == EPI_GATE_UP) {
-    const int P = wn * (NB / 2) + (nb >> 1);
     const int f = tn * (BN / 2) + P * 32 + c;
-    return ((nb & 1) ? a.B1 : a.B0) + (size_t)f * a.K;
+    return (blk ? a.B1 : a.B0) + (size_t)f * a.K;
   } else {
     return a.B0 + (size_t)(tn * BN + u) * a.K;
   }
@@ -122,11 +121,13 @@ __device__ __forceinline__ void epi_gate_up(const GemmArgs& a, int row, int tn, 
   a.act_out[(size_t)row * (a.N / 2) + f] = (bf16)(silu(g) * u);
 }
 
-template <int EPI, int BM, int BN>
+template <int EPI, int BM, int BN, int WM>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
-  constexpr int TM = BM / 2, TN = BN / 2, MB = TM / 32, NB = TN / 32;
+  constexpr int WN = 4 / WM;
+  constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
   constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
   constexpr int A_LOADS = A_BYTES / 1024 / 4, B_LOADS = BN * BK * 2 / 1024 / 4;
+  static_assert(MB >= 1 && NB >= 2 && A_LOADS >= 1, "tile shape");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -173,7 +174,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16{};
 
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   int arow[MB], brow[NB];
 #pragma unroll
   for (int i = 0; i < MB; ++i) arow[i] = wm * TM + i * 32 + (lane & 31);
@@ -301,18 +302,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
           if (ov > v || (ov == v && oi < idx)) { v = ov; idx = oi; }
         }
         if (c == 0 && row < a.M) {
-          a.part_val[(size_t)row * parts + tn * 2 + wn] = v;
-          a.part_idx[(size_t)row * parts + tn * 2 + wn] = idx;
+          a.part_val[(size_t)row * parts + tn * WN + wn] = v;
+          a.part_idx[(size_t)row * parts + tn * WN + wn] = idx;
         }
       }
   }
 }
 
-// Sum the K splits of a 128 x 128-tiled product in split order and apply the
-// epilogue.  Thread (row, group g of 64 virtual columns, lane column c) owns
-// virtual columns g*64 + c and g*64 + 32 + c: one rotary / gate-up pair (tile
-// g/2, pair g%2), or two residual columns.
-template <int EPI>
+// Sum the K splits in split order and apply the epilogue.  Thread (row,
+// group g of 64 virtual columns, lane column c) owns virtual columns g*64 + c
+// and g*64 + 32 + c: pair (g % (BN/64)) of tile g / (BN/64), or two residual
+// columns.
+template <int EPI, int BN>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
   const int half_n = a.N / 2;
@@ -325,68 +326,80 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
     x1 += a.partial[(size_t)s * a.M * a.N + base];
     x2 += a.partial[(size_t)s * a.M * a.N + base + 32];
   }
+  constexpr int PPT = BN / 64;     // pairs per tile
   if constexpr (EPI == EPI_RESID) {
     a.x[base] += x1;
     a.x[base + 32] += x2;
   } else if constexpr (EPI == EPI_QKV) {
-    epi_qkv<128>(a, row, g >> 1, g & 1, c, x1, x2);
+    epi_qkv<BN>(a, row, g / PPT, g % PPT, c, x1, x2);
   } else if constexpr (EPI == EPI_GATE_UP) {
-    epi_gate_up<128>(a, row, g >> 1, g & 1, c, x1, x2);
+    epi_gate_up<BN>(a, row, g / PPT, g % PPT, c, x1, x2);
   }
 }
 
-template <int EPI, int BM, int BN>
-hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
-  constexpr int SMEM = 2 * (BM + BN) * BK * 2;
-  static bool configured = false;
-  if (!configured) {
-    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
-    if (e != hipSuccess) return e;
-    configured = true;
-  }
-  const int grid = ((a.M + BM - 1) / BM) * (a.N / BN) * a.ksplit;
-  gemm_bf16_kernel<EPI, BM, BN><<<grid, NT, SMEM, s>>>(a);
-  if (a.ksplit > 1) {
-    const size_t threads = (size_t)a.M * (a.N / 2);
-    splitk_reduce_kernel<EPI><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
-  }
-  return hipGetLastError();
+enum TileShape { TILE_256x256, TILE_128x128, TILE_64x256, TILE_32x256 };
+
+// Shape choice: 256 x 256 tiles halve the operand traffic per flop but need
+// enough tiles to cover the CUs; few rows use 32- or 64-row tiles that stream
+// 256 weight rows each.  256-wide tiles need every weight segment (q/k/v) to
+// be a multiple of 256 so no tile straddles two.
+TileShape pick_tile(int M, int N, int n0, int n1) {
+  const bool w256 = N % 256 == 0 && n0 % 256 == 0 && n1 % 256 == 0;
+  if (w256 && M <= 32) return TILE_32x256;
+  if (w256 && M <= 64) return TILE_64x256;
+  if (w256 && M > 128 && (long)((M + 255) / 256) * (N / 256) >= 384) return TILE_256x256;
+  return TILE_128x128;
 }
 
-// 256 x 256 tiles (4 waves of 128 x 128) halve the operand traffic per flop
-// but need enough tiles to cover the 256 CUs; otherwise 128 x 128.  Weight
-// segments (q/k/v) must not straddle a tile.
-bool use_big_tiles(int M, int N, int n0, int n1) {
-  const long big_tiles = (long)((M + 255) / 256) * (N / 256);
-  return N % 256 == 0 && n0 % 256 == 0 && n1 % 256 == 0 && big_tiles >= 384;
-}
-
-// K splits for a 128 x 128-tiled product: enough work-groups for about two
-// per CU, at least 4 K steps per split, partials within the workspace area.
-int choose_splits(int epi, int M, int N, int K) {
-  if (epi == EPI_ARGMAX) return 1;
-  const long tiles = (long)((M + 127) / 128) * (N / 128);
-  if (tiles >= 384) return 1;
-  int s = (int)std::min<long>(8, (512 + tiles - 1) / tiles);
+// K splits: enough work-groups for about two per CU, at least 4 K steps per
+// split, partials within the workspace area.
+int choose_splits(int epi, long tiles, int M, int N, int K) {
+  if (epi == EPI_ARGMAX || tiles >= 384) return 1;
+  int s = (int)std::min<long>(16, (512 + tiles - 1) / tiles);
   const int kt = K / BK;
   while (s > 1 && (kt % s != 0 || kt / s < 4 || (size_t)s * M * N * 4 > kPartialCap)) --s;
   return s;
 }
 
-template <int EPI>
-hipError_t launch_epi(GemmArgs a, hipStream_t s) {
-  if (use_big_tiles(a.M, a.N, a.n0, a.n1)) {
-    a.ksplit = 1;
-    return launch_tile<EPI, 256, 256>(a, s);
+template <int EPI, int BM, int BN, int WM>
+hipError_t launch_tile(GemmArgs a, hipStream_t s) {
+  constexpr int SMEM = 2 * (BM + BN) * BK * 2;
+  static bool configured = false;
+  if (!configured) {
+    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN, WM>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
+    if (e != hipSuccess) return e;
+    configured = true;
   }
-  a.ksplit = a.partial ? choose_splits(EPI, a.M, a.N, a.K) : 1;
-  return launch_tile<EPI, 128, 128>(a, s);
+  const long tiles = (long)((a.M + BM - 1) / BM) * (a.N / BN);
+  a.ksplit = a.partial ? choose_splits(EPI, tiles, a.M, a.N, a.K) : 1;
+  gemm_bf16_kernel<EPI, BM, BN, WM><<<(unsigned)(tiles * a.ksplit), NT, SMEM, s>>>(a);
+  if (a.ksplit > 1) {
+    const size_t threads = (size_t)a.M * (a.N / 2);
+    splitk_reduce_kernel<EPI, BN><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
+  }
+  return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+  switch (pick_tile(a.M, a.N, a.n0, a.n1)) {
+    case TILE_256x256: return launch_tile<EPI, 256, 256, 2>(a, s);
+    case TILE_32x256: return launch_tile<EPI, 32, 256, 1>(a, s);
+    case TILE_64x256: return launch_tile<EPI, 64, 256, 2>(a, s);
+    default: return launch_tile<EPI, 128, 128, 2>(a, s);
+  }
 }
 
 }  // namespace
 
-int gemm_parts(int N, int M) { return use_big_tiles(M, N, N, 0) ? N / 128 : N / 64; }
+int gemm_parts(int N, int M) {
+  switch (pick_tile(M, N, N, 0)) {
+    case TILE_256x256: return N / 128;
+    case TILE_64x256: return N / 128;
+    default: return N / 64;       // 128x128 and 32x256: wave slabs of 64 columns
+  }
+}
 
 size_t gemm_partial_bytes() { return kPartialCap; }
 

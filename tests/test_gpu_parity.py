@@ -230,6 +230,24 @@ def test_two_layer_full_shape(name):
     release(ver, W_dev)
 
 
+@pytest.mark.parametrize("batch,budget", [(1, 1), (4, 8), (4, 16), (16, 4), (1, 64)])
+def test_two_layer_few_rows(batch, budget):
+    """8B shapes with 1 to 64 node rows: the skinny GEMM tiles (32 and 64
+    rows by 256 weight rows) and their K splits on every projection; a
+    64-node tree (256 query rows per KV head) takes the 8-wave attention."""
+    w = shallow(wl.sweep_workload(batch, budget))
+    say(f"{w.name}: 2-layer 8B-shape model, {w.n_tokens} nodes")
+    W_dev = wl.make_weights(w.cfg, 60 + budget, device="cuda")
+    W_cpu = cpu_weights(W_dev)
+    ver = device_setup(w, W_dev, seed=7)
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    check = sorted({0, w.batch - 1})
+    out, r, exc = full_check(w.cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check,
+                             envelope=True)
+    check_tree_kv(w.cfg, ver, ids, w.trees, lens, r, check, layers=1)
+    release(ver, W_dev)
+
+
 def test_llama1b_workload_parity():
     say("llama-1B shape: batch 32, KV U[512,2048], 15-node binary trees")
     w = wl.llama1b_workload(1000)
