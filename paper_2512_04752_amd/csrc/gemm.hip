@@ -17,7 +17,9 @@
 //   * operand tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 (no
 //     register staging) into a two-stage ring; the next K step is in flight
 //     while the current one is multiplied, and one barrier per K step both
-//     publishes the new stage and frees the old one;
+//     publishes the new stage and frees the old one.  A stage's wave-loads
+//     are issued in four quarters between MFMA blocks, with their LDS
+//     destinations in scalar registers;
 //   * each wave-load writes 1 KB = 8 tile rows of 128 bytes; the 16-byte chunk
 //     index of row r is XOR-ed with (r >> 1) & 7, which makes the MFMA operand
 //     reads (16 consecutive rows, one chunk) hit all 64 LDS banks once;
@@ -130,7 +132,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   static_assert(MB >= 1 && NB >= 2 && A_LOADS >= 1, "tile shape");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // The wave index is made scalar so that every LDS destination (M0) of the
+  // direct loads is computed in scalar registers.
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ntm = (a.M + BM - 1) / BM;
   const int tiles = ntm * (a.N / BN);
   const int total = gridDim.x;
@@ -159,13 +163,16 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
     const int trow = (wave * B_LOADS + j) * 8 + lr;
     pb[j] = weight_row<EPI, BN>(a, tn, trow) + k_off + (((lane & 7) ^ swz(trow)) << 3);
   }
-  auto issue = [&](int kt, int slot) {
+  // Quarter q of stage kt's loads (every fourth wave-load), so that a stage's
+  // loads are spread between MFMA blocks instead of issued in one burst.
+  auto issue_q = [&](int kt, int slot, int q) {
     char* base = smem + slot * STAGE;
 #pragma unroll
-    for (int j = 0; j < A_LOADS; ++j) load_lds16(pa[j] + kt * BK, base + (wave * A_LOADS + j) * 1024);
+    for (int j = 0; j < A_LOADS; ++j)
+      if (j % 4 == q) load_lds16(pa[j] + kt * BK, base + (wave * A_LOADS + j) * 1024);
 #pragma unroll
     for (int j = 0; j < B_LOADS; ++j)
-      load_lds16(pb[j] + kt * BK, base + A_BYTES + (wave * B_LOADS + j) * 1024);
+      if (j % 4 == q) load_lds16(pb[j] + kt * BK, base + A_BYTES + (wave * B_LOADS + j) * 1024);
   };
 
   f32x16 acc[MB][NB];
@@ -199,25 +206,41 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
   };
 
-  issue(0, 0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) issue_q(0, 0, q);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  if (KT > 1) issue(1, 1);
+  // Stage pk (slot ps) has quarters 1..3 still to issue, one before each of
+  // the next three MFMA blocks; -1 when none.
+  int pk = -1, ps = 0;
+  if (KT > 1) {
+    issue_q(1, 1, 0);
+    pk = 1;
+    ps = 1;
+  }
   load_frags(smem, 0, 0);
   for (int kt = 0; kt < KT; ++kt) {
     const char* st = smem + (kt & 1) * STAGE;
     load_frags(st, 1, 1);
+    if (pk >= 0) issue_q(pk, ps, 1);
     mfmas(0);
     load_frags(st, 2, 0);
+    if (pk >= 0) issue_q(pk, ps, 2);
     mfmas(1);
     load_frags(st, 3, 1);
+    if (pk >= 0) issue_q(pk, ps, 3);
     mfmas(0);
+    pk = -1;
     if (kt + 1 < KT) {
       // Stage kt+1 has landed for every wave, and every wave is done reading
       // stage kt (its last fragments are in registers): refill that slot.
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
-      if (kt + 2 < KT) issue(kt + 2, kt & 1);
+      if (kt + 2 < KT) {
+        issue_q(kt + 2, kt & 1, 0);
+        pk = kt + 2;
+        ps = kt & 1;
+      }
       load_frags(smem + ((kt + 1) & 1) * STAGE, 0, 0);
     }
     mfmas(1);
