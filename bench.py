@@ -38,6 +38,9 @@ def parse():
                    help="early | tail | llama1b | sweep_b<B>_n<n> (one strategy-cost sweep cell)")
     p.add_argument("--cpu-baseline", type=int, default=1, help="0 skips the oracle timing")
     p.add_argument("--seed", type=int, default=None)
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                   help="only copy BYTES device-to-device 5 times (a reference for the HBM "
+                        "byte counters) and exit")
     p.add_argument("--sweep", default=None, metavar="OUT.jsonl",
                    help="run the strategy-cost sweep (batch x tree budget) and write one JSON "
                         "line per cell to OUT.jsonl")
@@ -118,6 +121,38 @@ def run_sweep(args, out_path):
     return rows
 
 
+def recorded_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    copy-calibrated rocprofv3 counter summary, or None when there is none or
+    the kernel's source has changed since the counters were taken."""
+    import glob
+    import hashlib
+    for path in glob.glob(os.path.join(ROOT, "profiles", "hbm_traffic__*.md")):
+        for line in open(path):
+            f = line.split()
+            if len(f) != 6 or f[0] != "traffic" or f[1] != workload or f[2] != kernel:
+                continue
+            kv = dict(x.split("=", 1) for x in f[3:])
+            src = os.path.join(ROOT, kv["source"])
+            if os.path.exists(src) and hashlib.sha1(open(src, "rb").read()).hexdigest() == kv["sha1"]:
+                return int(float(kv["bytes_per_launch"]))
+    return None
+
+
+def attention_kernels(cfg, w):
+    """Kernels one attention launch runs for this workload's tree sizes."""
+    G = cfg.n_heads // cfg.n_kv_heads
+    tiles = [(len(t[0]) * G + 31) // 32 for t in w.trees]
+    names = []
+    if min(tiles) == 1:
+        names.append(f"tree_attention_kernel<{cfg.head_dim}>")
+    if any(1 < t <= 4 for t in tiles):
+        names.append(f"tree_attention_wide_kernel<{cfg.head_dim},4>")
+    if max(tiles) > 4:
+        names.append(f"tree_attention_wide_kernel<{cfg.head_dim},8>")
+    return names
+
+
 def make_workload(name, seed):
     import workload as wl
     m = re.fullmatch(r"sweep_b(\d+)_n(\d+)", name)
@@ -156,6 +191,15 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        src = torch.ones(args.copy_calibration, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": args.copy_calibration, "copies": 5}), flush=True)
+        return
     if args.sweep:
         rows = run_sweep(args, args.sweep)
         best = max(rows, key=lambda r: r["accepted_tokens_per_s"])
@@ -242,13 +286,15 @@ def main():
             gu_bytes / (PEAK_HBM_GBS * 1e9):
         achieved = gu_flops / (avg_ms / 1e3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": recorded_traffic(args.workload, "gemm_bf16_kernel<EPI_GATE_UP>"),
                 "kernel": "gemm_bf16_kernel<EPI_GATE_UP>",
                 "work_per_launch": f"2*{n_tok}*{2 * F}*{H} flop"}
     elif dominant == "gemm_gate_up":
         achieved = gu_bytes / (avg_ms / 1e3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                "traffic": recorded_traffic(args.workload, "gemm_bf16_kernel<EPI_GATE_UP>"),
                 "kernel": "gemm_bf16_kernel<EPI_GATE_UP> (+ split-K reduce)",
                 "work_per_launch": f"{gu_bytes} bytes (gate and up weights once, rows in and out)"}
     else:
@@ -257,9 +303,11 @@ def main():
         qo_bytes = n_tok * cfg.n_heads * d * 2 * 2
         work = kv_bytes + qo_bytes
         achieved = work / (avg_ms / 1e3) / 1e9
+        kern = " + ".join(attention_kernels(cfg, w) + [f"attention_combine_kernel<{d}>"])
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
-                "kernel": "tree_attention_kernel<128> + attention_combine_kernel<128>",
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                "traffic": recorded_traffic(args.workload, kern.replace(" ", "")),
+                "kernel": kern,
                 "work_per_launch": f"{work} bytes (K/V of every key once, q in, o out)"}
     roof["avg_launch_ms"] = round(avg_ms, 5)
     roof["launches"] = dom_launches
@@ -297,8 +345,9 @@ def main():
 
 
 def cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok, ms_per_step):
-    """The oracle, untuned, on the host cores over a bounded sample: the first
-    sample(s) of the same workload with their unsteered draft trees."""
+    """The oracle, untuned, on the host cores over a bounded sample: the
+    workload's samples in order, with their unsteered draft trees, one verify
+    call each, until about 10 s of CPU time (at most 30 s, at most 16 samples)."""
     import torch
 
     import oracle
@@ -306,18 +355,22 @@ def cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok, ms_per_step):
     Wc = {"tok_embed": W["tok_embed"].cpu(), "final_norm": W["final_norm"].cpu(),
           "lm_head": W["lm_head"].cpu(),
           "layers": [{k: v.cpu() for k, v in lw.items()} for lw in W["layers"]]}
-    n_s = 1 if cfg.hidden == 4096 else 2
-    sel = list(range(n_s))
-    pk = [ver.kv.sample_view(b)[0][:, :, :lens[b]].cpu() for b in sel]
-    pv = [ver.kv.sample_view(b)[1][:, :, :lens[b]].cpu() for b in sel]
-    t0 = time.perf_counter()
-    oracle.verify(cfg, Wc, pk, pv, [lens[b] for b in sel], [plain_trees[b] for b in sel])
-    dt = time.perf_counter() - t0
-    toks = sum(len(plain_trees[b][0]) for b in sel)
+    dt, toks, used = 0.0, 0, []
+    for b in range(min(16, w.batch)):
+        pk = [ver.kv.sample_view(b)[0][:, :, :lens[b]].cpu()]
+        pv = [ver.kv.sample_view(b)[1][:, :, :lens[b]].cpu()]
+        t0 = time.perf_counter()
+        oracle.verify(cfg, Wc, pk, pv, [lens[b]], [plain_trees[b]])
+        dt += time.perf_counter() - t0
+        toks += len(plain_trees[b][0])
+        used.append(b)
+        if dt >= 10.0 or dt * (len(used) + 1) / len(used) > 30.0:
+            break
     return {"value": round(toks / dt, 4), "unit": "tokens/s", "cores": torch.get_num_threads(),
             "kind": "oracle",
-            "sample": f"{n_s} sample(s) of the same workload ({toks} tree nodes, KV lengths "
-                      f"{[lens[b] for b in sel]}), float64 torch-CPU oracle, {dt:.1f} s"}
+            "sample": f"{len(used)} sample(s) of the same workload, one verify call each ({toks} tree "
+                      f"nodes, KV lengths {[lens[b] for b in used]}), float64 torch-CPU oracle, "
+                      f"{dt:.1f} s"}
 
 
 if __name__ == "__main__":
