@@ -22,8 +22,9 @@
 //
 // The softmax runs in the base-2 domain (scores scaled by log2(e)/sqrt(d)
 // inside one FMA, v_exp_f32 directly).  The running output is rescaled only
-// when some row's maximum grew in this block (a wave-uniform test); with a
-// long prefix the maximum settles early and most blocks skip the rescale.
+// when some row's maximum outgrew the reference maximum by more than
+// kRescaleSlack (a wave-uniform test); the maximum settles within that slack
+// after the first blocks, so the rescale of the accumulators is rare.
 //
 //   * tree_attention_kernel: one 32-row tile per work-group (at most 32 query
 //     rows per KV head, e.g. 8-node trees with 4 query heads per KV head).  The
@@ -73,6 +74,14 @@ __device__ __forceinline__ void wait_vm() {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// The running output is kept relative to a reference maximum m_run and
+// rescaled only when some row's maximum exceeds it by more than this many
+// binary orders; meanwhile probabilities up to 2^kRescaleSlack are formed,
+// which fp32 sums and bf16 P^T operands hold with unchanged relative
+// precision.  Softmax is invariant to the reference, so the result is the
+// same up to rounding.
+constexpr float kRescaleSlack = 8.f;
+
 // max / sum of a value and its copy in lane ^ 32 (v_permlane32_swap: each
 // lane ends with both halves' values in the two results).
 __device__ __forceinline__ float max_xor32(float x) {
@@ -112,7 +121,7 @@ __device__ __forceinline__ void softmax_stage(bool mask_a, bool mask_b, f32x16& 
   for (int e = 1; e < 16; ++e) smax = fmaxf(smax, fmaxf(sa[e], sb[e]));
   smax = max_xor32(smax);
   const float m_new = fmaxf(m_run, smax * sl2);
-  if (__ballot(m_new > m_run)) {
+  if (__ballot(m_new > m_run + kRescaleSlack)) {
     const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
     l_run *= alpha;
 #pragma unroll
@@ -181,12 +190,11 @@ __device__ __forceinline__ void softmax_block(f32x16& s, int kb, int key1, int s
   float smax = s[0];
 #pragma unroll
   for (int e = 1; e < 16; ++e) smax = fmaxf(smax, s[e]);
-  smax = fmaxf(smax, __shfl_xor(smax, 32));
+  smax = max_xor32(smax);
   const float m_new = fmaxf(m_run, smax * sl2);
-  if (__ballot(m_new > m_run)) {
-    // exp2(m_run - m_new) is 0 for a first visible block (m_run = -inf) and
-    // 1 for rows whose maximum did not move; rows with nothing visible yet
-    // keep alpha = 1.
+  if (__ballot(m_new > m_run + kRescaleSlack)) {
+    // exp2(m_run - m_new) is 0 for a first visible block (m_run = -inf);
+    // rows with nothing visible yet keep alpha = 1.
     const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
     l_run *= alpha;
 #pragma unroll
@@ -300,7 +308,7 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
   const AttnItem it = a.items[item];
   if (it.sample < 0) return;          // padding of a shorter per-XCD list
   const SampleInfo si = a.samples[it.sample];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 31, h = lane >> 5;
   const int G = a.n_heads / a.n_kv_heads;
   const int nq_hd = a.n_heads * HD;
@@ -452,7 +460,7 @@ __global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void tree_attention_wide_
   const AttnItem it = items[item];
   if (it.sample < 0) return;
   const SampleInfo si = a.samples[it.sample];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 31, h = lane >> 5;
   const int G = a.n_heads / a.n_kv_heads;
   const int nq_hd = a.n_heads * HD;
