@@ -569,7 +569,7 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     g.logits = D.logits;
     HIP_TRY(timed(SPEC_K_LM_HEAD, s, [&] { return launch_gemm(EPI_ARGMAX, g, s); }), "lm head");
   }
-  HIP_TRY(launch_argmax_reduce(d_lmv, d_lmi, N, gemm_parts(V, N), d_arg, D.argmax, s), "argmax");
+  HIP_TRY(launch_argmax_reduce(d_lmv, d_lmi, N, gemm_parts(V, N, H), d_arg, D.argmax, s), "argmax");
   HIP_TRY(launch_accept(d_si, batch, d_tok, d_par, d_toks, d_arg, accepted_len, next_token,
                         accepted_nodes, s),
           "accept");

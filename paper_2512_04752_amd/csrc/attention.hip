@@ -72,6 +72,15 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Work-group barrier for a shared LDS ring: this wave's LDS reads are
+// complete (the oldest slot may be refilled by any wave afterwards) while its
+// direct-to-LDS loads of later stages stay in flight.  __syncthreads() would
+// add a work-group fence, i.e. a wait for every outstanding global load,
+// leaving one stage of lookahead however deep the ring.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // The running output is kept relative to a reference maximum m_run and
@@ -526,7 +535,7 @@ __global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void tree_attention_wide_
       } else {
         wait_vm<0>();
       }
-      __syncthreads();    // stage t visible to all waves; stage t-1 fully consumed
+      ring_barrier();     // stage t visible to all waves; stage t-1 fully consumed
       if (t + NS - 1 < nstage) issue(t + NS - 1, (u + NS - 1) % NS);
       const char* st = smem + u * C::W_STAGE;
       const int kb = it.key0 + t * C::WKEYS;

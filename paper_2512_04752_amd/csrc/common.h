@@ -77,7 +77,7 @@ struct GemmArgs {
   // EPI_GATE_UP
   bf16* act_out;          // [M][ffn]
   // EPI_ARGMAX
-  float* part_val;        // [M][gemm_parts(N, M)]
+  float* part_val;        // [M][gemm_parts(N, M, K)]
   int32_t* part_idx;
   float* logits;          // optional [M][N]
   // Split-K scratch (gemm_partial_bytes() bytes; NULL disables splitting) and
@@ -88,8 +88,8 @@ struct GemmArgs {
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 // Number of (max, index) partials per row the EPI_ARGMAX launch for an
-// [M x N] product writes.
-int gemm_parts(int N, int M);
+// [M x N] product with inner dimension K writes.
+int gemm_parts(int N, int M, int K);
 // Bytes of split-K partial storage launch_gemm may use through GemmArgs::partial.
 size_t gemm_partial_bytes();
 

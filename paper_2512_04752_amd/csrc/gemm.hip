@@ -15,21 +15,24 @@
 // tile BM x BN, each wave BM/WM x BN/WN built from 32 x 32
 // v_mfma_f32_32x32x16_bf16 blocks; K step 64):
 //   * operand tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 (no
-//     register staging) into a two-stage ring; the next K step is in flight
-//     while the current one is multiplied, and one barrier per K step both
-//     publishes the new stage and frees the old one.  A stage's wave-loads
-//     are issued in four quarters between MFMA blocks, with their LDS
-//     destinations in scalar registers;
+//     register staging) into a ring of NS stages; the next NS-1 K steps are
+//     in flight while the current one is multiplied, and one barrier per K
+//     step both publishes the next stage and frees the oldest slot.  The
+//     barrier waits only for this wave's LDS reads and for the loads of the
+//     next stage (vmcnt counts the later stages out), never for the whole
+//     ring.  A stage's wave-loads are issued in four quarters between MFMA
+//     blocks, with their LDS destinations in scalar registers;
 //   * each wave-load writes 1 KB = 8 tile rows of 128 bytes; the 16-byte chunk
 //     index of row r is XOR-ed with (r >> 1) & 7, which makes the MFMA operand
 //     reads (16 consecutive rows, one chunk) hit all 64 LDS banks once;
 //   * fragments of the next 16-wide k-step are read from LDS into a second
 //     register set while the current set feeds the MFMAs.
-// Tile shapes: 256 x 256 (4 waves of 128 x 128) when the product has enough
-// tiles for the 256 CUs, 128 x 128 otherwise, and 32 x 256 / 64 x 256 for few
-// rows, where the weights are streamed and the rows are few.  Work-groups are
-// dealt round-robin over the 8 XCDs; the tile order is remapped so that the M
-// tiles sharing one weight tile run on one XCD and hit its L2.
+// Tile shapes (pick_tile): 256 x 256 (4 waves of 128 x 128, 2 stages) and
+// 256 x 128 (128 x 64 per wave, 3 stages) for many rows, 128 x 128 (2 or 4
+// stages) for up to 128 rows or narrow products, and 32 x 256 / 64 x 256 (3
+// stages) for few rows, where the weights are streamed and the rows are few.  Work-groups are dealt round-robin over the
+// 8 XCDs; the tile order is remapped so that the M tiles sharing one weight
+// tile run on one XCD and hit its L2.
 //
 // Products with too few output tiles to fill the CUs split K: each split
 // writes its fp32 tile to a partial buffer and a second kernel sums the splits
@@ -52,6 +55,21 @@ __device__ __forceinline__ void load_lds16(const void* g, void* lds) {
 }
 
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Work-group barrier for the LDS ring: this wave's LDS reads are complete
+// (its slot may be refilled by any wave afterwards), but its direct-to-LDS
+// loads of later stages stay in flight.  __syncthreads() would add a
+// work-group fence, i.e. a wait for every outstanding global load, which
+// would leave only one stage of lookahead however deep the ring.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // Virtual-column mapping.  Column u of an output tile belongs to wave column
 // wn = u / TN, MFMA block nb = (u % TN) / 32, lane column c = u % 32.  For
@@ -123,13 +141,15 @@ __device__ __forceinline__ void epi_gate_up(const GemmArgs& a, int row, int tn, 
   a.act_out[(size_t)row * (a.N / 2) + f] = (bf16)(silu(g) * u);
 }
 
-template <int EPI, int BM, int BN, int WM>
+template <int EPI, int BM, int BN, int WM, int NS>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int WN = 4 / WM;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
   constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
   constexpr int A_LOADS = A_BYTES / 1024 / 4, B_LOADS = BN * BK * 2 / 1024 / 4;
+  constexpr int LPW = A_LOADS + B_LOADS;    // wave-loads per wave and stage
   static_assert(MB >= 1 && NB >= 2 && A_LOADS >= 1, "tile shape");
+  static_assert(NS >= 2 && (NS - 2) * LPW <= 63, "ring depth (vmcnt holds at most 63)");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   // The wave index is made scalar so that every LDS destination (M0) of the
@@ -206,21 +226,23 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
   };
 
+  // Prologue: stages 0 .. NS-2 in flight, wait for stage 0.
 #pragma unroll
-  for (int q = 0; q < 4; ++q) issue_q(0, 0, q);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  // Stage pk (slot ps) has quarters 1..3 still to issue, one before each of
-  // the next three MFMA blocks; -1 when none.
-  int pk = -1, ps = 0;
-  if (KT > 1) {
-    issue_q(1, 1, 0);
-    pk = 1;
-    ps = 1;
-  }
+  for (int st = 0; st < NS - 1; ++st)
+    if (st < KT) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) issue_q(st, st, q);
+    }
+  if (KT >= NS - 1) wait_vm<(NS - 2) * LPW>();
+  else wait_vm<0>();
+  ring_barrier();
+  // Stage pk (slot ps) is issued quarter by quarter between the MFMA blocks
+  // of the current step; -1 when none is left.
+  int pk = NS - 1 < KT ? NS - 1 : -1, ps = NS - 1;
+  if (pk >= 0) issue_q(pk, ps, 0);
   load_frags(smem, 0, 0);
   for (int kt = 0; kt < KT; ++kt) {
-    const char* st = smem + (kt & 1) * STAGE;
+    const char* st = smem + (kt % NS) * STAGE;
     load_frags(st, 1, 1);
     if (pk >= 0) issue_q(pk, ps, 1);
     mfmas(0);
@@ -232,16 +254,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
     mfmas(0);
     pk = -1;
     if (kt + 1 < KT) {
-      // Stage kt+1 has landed for every wave, and every wave is done reading
-      // stage kt (its last fragments are in registers): refill that slot.
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-      if (kt + 2 < KT) {
-        issue_q(kt + 2, kt & 1, 0);
-        pk = kt + 2;
-        ps = kt & 1;
+      // Stage kt+1 has landed for every wave (stages kt+2 .. kt+NS-1 may
+      // still be in flight), and every wave is done reading stage kt (its
+      // last fragments are in registers): that slot takes stage kt+NS.
+      if (kt + NS - 1 < KT) wait_vm<(NS - 2) * LPW>();
+      else wait_vm<0>();
+      ring_barrier();
+      if (kt + NS < KT) {
+        pk = kt + NS;
+        ps = kt % NS;
+        issue_q(pk, ps, 0);
       }
-      load_frags(smem + ((kt + 1) & 1) * STAGE, 0, 0);
+      load_frags(smem + ((kt + 1) % NS) * STAGE, 0, 0);
     }
     mfmas(1);
   }
@@ -360,43 +384,58 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   }
 }
 
-enum TileShape { TILE_256x256, TILE_128x128, TILE_64x256, TILE_32x256 };
+enum TileShape { TILE_256x256, TILE_256x128, TILE_128x128_2WG, TILE_128x128, TILE_64x256, TILE_32x256 };
 
-// Shape choice: 256 x 256 tiles halve the operand traffic per flop but need
-// enough tiles to cover the CUs; few rows use 32- or 64-row tiles that stream
-// 256 weight rows each.  256-wide tiles need every weight segment (q/k/v) to
-// be a multiple of 256 so no tile straddles two.
-TileShape pick_tile(int M, int N, int n0, int n1) {
+// Shape choice (measured over the verify step's products at 32 to 1024 rows):
+//   * few rows: 32- or 64-row tiles that stream 256 weight rows each;
+//   * up to 128 rows: 128 x 128 tiles with a 4-stage ring (one work-group per
+//     CU, deep lookahead for the weight stream);
+//   * many rows and at least 384 256 x 256 tiles (gate/up, LM head): 256 x 256
+//     tiles, whose 2-stage ring fills the LDS; they need the fewest operand
+//     bytes per flop;
+//   * the q/k/v projection at 512 rows and more: 128 x 128 tiles with a
+//     2-stage ring, two work-groups per CU, so that one group's epilogue
+//     (rotary, scattered cache writes) overlaps the other's main loop;
+//   * otherwise 256 x 128 tiles with a 3-stage ring, or, for products too
+//     narrow to give 64 of them, 128 x 128 tiles with split K.
+// 256-wide tiles need every weight segment (q/k/v) to be a multiple of 256 so
+// no tile straddles two; 128-wide ones need multiples of 128.
+TileShape pick_tile(int epi, int M, int N, int K, int n0, int n1) {
   const bool w256 = N % 256 == 0 && n0 % 256 == 0 && n1 % 256 == 0;
   if (w256 && M <= 32) return TILE_32x256;
   if (w256 && M <= 64) return TILE_64x256;
+  if (M <= 128) return TILE_128x128;
   if (w256 && M > 128 && (long)((M + 255) / 256) * (N / 256) >= 384) return TILE_256x256;
-  return TILE_128x128;
+  if (epi == EPI_QKV && M >= 512) return TILE_128x128_2WG;
+  if ((long)((M + 255) / 256) * (N / 128) < 64 && K <= 4096) return TILE_128x128;
+  return TILE_256x128;
 }
 
-// K splits: enough work-groups for about two per CU, at least 4 K steps per
-// split, partials within the workspace area.
-int choose_splits(int epi, long tiles, int M, int N, int K) {
-  if (epi == EPI_ARGMAX || tiles >= 384) return 1;
-  int s = (int)std::min<long>(16, (512 + tiles - 1) / tiles);
+// K splits: about one work-group per CU for the wide tiles (their ring holds
+// a CU's LDS) and two for the skinny ones, at least 8 K steps per split, the
+// splits dividing the K steps, partials within the workspace area.
+int choose_splits(int epi, int BM, long tiles, int M, int N, int K) {
+  if (epi == EPI_ARGMAX) return 1;
+  const long target = BM <= 64 ? 512 : 256;
+  int s = (int)std::max<long>(1, std::min<long>(16, target / tiles));
   const int kt = K / BK;
-  while (s > 1 && (kt % s != 0 || kt / s < 4 || (size_t)s * M * N * 4 > kPartialCap)) --s;
+  while (s > 1 && (kt % s != 0 || kt / s < 8 || (size_t)s * M * N * 4 > kPartialCap)) --s;
   return s;
 }
 
-template <int EPI, int BM, int BN, int WM>
+template <int EPI, int BM, int BN, int WM, int NS>
 hipError_t launch_tile(GemmArgs a, hipStream_t s) {
-  constexpr int SMEM = 2 * (BM + BN) * BK * 2;
+  constexpr int SMEM = NS * (BM + BN) * BK * 2;
   static bool configured = false;
   if (!configured) {
-    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN, WM>,
+    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN, WM, NS>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
     if (e != hipSuccess) return e;
     configured = true;
   }
   const long tiles = (long)((a.M + BM - 1) / BM) * (a.N / BN);
-  a.ksplit = a.partial ? choose_splits(EPI, tiles, a.M, a.N, a.K) : 1;
-  gemm_bf16_kernel<EPI, BM, BN, WM><<<(unsigned)(tiles * a.ksplit), NT, SMEM, s>>>(a);
+  a.ksplit = a.partial ? choose_splits(EPI, BM, tiles, a.M, a.N, a.K) : 1;
+  gemm_bf16_kernel<EPI, BM, BN, WM, NS><<<(unsigned)(tiles * a.ksplit), NT, SMEM, s>>>(a);
   if (a.ksplit > 1) {
     const size_t threads = (size_t)a.M * (a.N / 2);
     splitk_reduce_kernel<EPI, BN><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
@@ -406,21 +445,23 @@ hipError_t launch_tile(GemmArgs a, hipStream_t s) {
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  switch (pick_tile(a.M, a.N, a.n0, a.n1)) {
-    case TILE_256x256: return launch_tile<EPI, 256, 256, 2>(a, s);
-    case TILE_32x256: return launch_tile<EPI, 32, 256, 1>(a, s);
-    case TILE_64x256: return launch_tile<EPI, 64, 256, 2>(a, s);
-    default: return launch_tile<EPI, 128, 128, 2>(a, s);
+  switch (pick_tile(EPI, a.M, a.N, a.K, a.n0, a.n1)) {
+    case TILE_256x256: return launch_tile<EPI, 256, 256, 2, 2>(a, s);
+    case TILE_256x128: return launch_tile<EPI, 256, 128, 2, 3>(a, s);
+    case TILE_128x128_2WG: return launch_tile<EPI, 128, 128, 2, 2>(a, s);
+    case TILE_32x256: return launch_tile<EPI, 32, 256, 1, 3>(a, s);
+    case TILE_64x256: return launch_tile<EPI, 64, 256, 2, 3>(a, s);
+    default: return launch_tile<EPI, 128, 128, 2, 4>(a, s);
   }
 }
 
 }  // namespace
 
-int gemm_parts(int N, int M) {
-  switch (pick_tile(M, N, N, 0)) {
+int gemm_parts(int N, int M, int K) {
+  switch (pick_tile(EPI_ARGMAX, M, N, K, N, 0)) {
     case TILE_256x256: return N / 128;
     case TILE_64x256: return N / 128;
-    default: return N / 64;       // 128x128 and 32x256: wave slabs of 64 columns
+    default: return N / 64;       // 256x128, 128x128 and 32x256: wave slabs of 64 columns
   }
 }
 
