@@ -13,26 +13,27 @@
 //
 // Structure (one 256-thread work-group = 4 waves in a WM x WN grid, output
 // tile BM x BN, each wave BM/WM x BN/WN built from 32 x 32
-// v_mfma_f32_32x32x16_bf16 blocks; K step 64):
+// v_mfma_f32_32x32x16_bf16 blocks; K step BK = 64 or 32):
 //   * operand tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 (no
 //     register staging) into a ring of NS stages; the next NS-1 K steps are
 //     in flight while the current one is multiplied, and one barrier per K
 //     step both publishes the next stage and frees the oldest slot.  The
 //     barrier waits only for this wave's LDS reads and for the loads of the
 //     next stage (vmcnt counts the later stages out), never for the whole
-//     ring.  A stage's wave-loads are issued in four quarters between MFMA
+//     ring.  A stage's wave-loads are issued in BK/16 parts between the MFMA
 //     blocks, with their LDS destinations in scalar registers;
-//   * each wave-load writes 1 KB = 8 tile rows of 128 bytes; the 16-byte chunk
-//     index of row r is XOR-ed with (r >> 1) & 7, which makes the MFMA operand
-//     reads (16 consecutive rows, one chunk) hit all 64 LDS banks once;
+//   * each wave-load writes 1 KB = 8 tile rows of 128 bytes (16 of 64 bytes
+//     for BK = 32); the 16-byte chunk index of row r is XOR-ed with
+//     (r >> 1) & 7 ((r >> 2) & 3), which makes the MFMA operand reads (16
+//     consecutive rows, one chunk) hit all 64 LDS banks once;
 //   * fragments of the next 16-wide k-step are read from LDS into a second
 //     register set while the current set feeds the MFMAs.
-// Tile shapes (pick_tile): 256 x 256 (4 waves of 128 x 128, 2 stages) and
-// 256 x 128 (128 x 64 per wave, 3 stages) for many rows, 128 x 128 (2 or 4
-// stages) for up to 128 rows or narrow products, and 32 x 256 / 64 x 256 (3
-// stages) for few rows, where the weights are streamed and the rows are few.  Work-groups are dealt round-robin over the
-// 8 XCDs; the tile order is remapped so that the M tiles sharing one weight
-// tile run on one XCD and hit its L2.
+// Tile shapes (pick_tile): 256 x 256 (4 waves of 128 x 128, 4 stages of 32)
+// and 256 x 128 (128 x 64 per wave, 3 stages) for many rows, 128 x 128 (2 or
+// 4 stages) for up to 128 rows or narrow products, and 32 x 256 / 64 x 256
+// (3 stages) for few rows, where the weights are streamed.  Work-groups are
+// dealt round-robin over the 8 XCDs; the tile order is remapped so that the
+// M tiles sharing one weight tile run on one XCD and hit its L2.
 //
 // Products with too few output tiles to fill the CUs split K: each split
 // writes its fp32 tile to a partial buffer and a second kernel sums the splits
@@ -45,7 +46,7 @@ namespace spec {
 
 namespace {
 
-constexpr int BK = 64, NT = 256;
+constexpr int NT = 256;
 constexpr size_t kPartialCap = 64ull << 20;   // bytes of split-K partials (workspace)
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -54,7 +55,11 @@ __device__ __forceinline__ void load_lds16(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
 }
 
-__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+// 16-byte chunk swizzle of tile row `row` for K steps of BK elements (rows of
+// 2*BK bytes): 16 consecutive rows reading one logical chunk hit 16
+// distinct 16-byte bank groups.
+template <int BK>
+__device__ __forceinline__ int swz(int row) { return BK == 64 ? (row >> 1) & 7 : (row >> 2) & 3; }
 
 // Wait until at most N vector-memory operations of this wave are in flight.
 template <int N>
@@ -141,13 +146,25 @@ __device__ __forceinline__ void epi_gate_up(const GemmArgs& a, int row, int tn, 
   a.act_out[(size_t)row * (a.N / 2) + f] = (bf16)(silu(g) * u);
 }
 
-template <int EPI, int BM, int BN, int WM, int NS>
-__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
+// Work-groups per CU a tile configuration is compiled for: two when its ring
+// leaves room for a second one in the 160 KB of LDS and its accumulators
+// leave room for a second wave per SIMD, so that one wave's waits are
+// covered by the other's MFMAs.
+template <int BM, int BN, int NS, int BK>
+constexpr int gemm_occupancy() {
+  return (NS * (BM + BN) * BK * 2 <= 80 * 1024 && BM * BN <= 256 * 128) ? 2 : 1;
+}
+
+template <int EPI, int BM, int BN, int WM, int NS, int BK>
+__global__ __launch_bounds__(NT, (gemm_occupancy<BM, BN, NS, BK>())) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int WN = 4 / WM;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
-  constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
-  constexpr int A_LOADS = A_BYTES / 1024 / 4, B_LOADS = BN * BK * 2 / 1024 / 4;
+  constexpr int ROWB = BK * 2, CPR = BK / 8, RPL = 1024 / ROWB;  // row bytes, chunks, rows per load
+  constexpr int KS = BK / 16;                                     // MFMA k-steps per K step
+  constexpr int A_BYTES = BM * ROWB, STAGE = (BM + BN) * ROWB;
+  constexpr int A_LOADS = A_BYTES / 1024 / 4, B_LOADS = BN * ROWB / 1024 / 4;
   constexpr int LPW = A_LOADS + B_LOADS;    // wave-loads per wave and stage
+  static_assert(BK == 32 || BK == 64, "K step");
   static_assert(MB >= 1 && NB >= 2 && A_LOADS >= 1, "tile shape");
   static_assert(NS >= 2 && (NS - 2) * LPW <= 63, "ring depth (vmcnt holds at most 63)");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
@@ -165,34 +182,35 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   const int KT = a.K / BK / a.ksplit;            // K steps of this split
   const int k_off = split * KT * BK;
 
-  // Wave-load j of this wave fills tile rows [(wave*LOADS + j)*8, +8); lane l
-  // lands at row l/8, physical chunk l%8, so it fetches logical chunk
-  // (l%8) ^ swz(row).
-  const int lr = lane >> 3;
+  // Wave-load j of this wave fills tile rows [(wave*LOADS + j)*RPL, +RPL);
+  // lane l lands at row l/CPR, physical chunk l%CPR, so it fetches logical
+  // chunk (l%CPR) ^ swz(row).
+  const int lr = lane / CPR, lc = lane % CPR;
   const bf16* pa[A_LOADS];
   const bf16* pb[B_LOADS];
 #pragma unroll
   for (int j = 0; j < A_LOADS; ++j) {
-    const int trow = (wave * A_LOADS + j) * 8 + lr;
+    const int trow = (wave * A_LOADS + j) * RPL + lr;
     int row = tm * BM + trow;
     row = row < a.M ? row : a.M - 1;      // rows past M repeat the last row; never stored
-    pa[j] = a.A + (size_t)row * a.K + k_off + (((lane & 7) ^ swz(trow)) << 3);
+    pa[j] = a.A + (size_t)row * a.K + k_off + ((lc ^ swz<BK>(trow)) << 3);
   }
 #pragma unroll
   for (int j = 0; j < B_LOADS; ++j) {
-    const int trow = (wave * B_LOADS + j) * 8 + lr;
-    pb[j] = weight_row<EPI, BN>(a, tn, trow) + k_off + (((lane & 7) ^ swz(trow)) << 3);
+    const int trow = (wave * B_LOADS + j) * RPL + lr;
+    pb[j] = weight_row<EPI, BN>(a, tn, trow) + k_off + ((lc ^ swz<BK>(trow)) << 3);
   }
-  // Quarter q of stage kt's loads (every fourth wave-load), so that a stage's
-  // loads are spread between MFMA blocks instead of issued in one burst.
+  // Part q of stage kt's loads (every KS-th wave-load), so that a stage's
+  // loads are spread between the MFMA blocks of a K step instead of issued
+  // in one burst.
   auto issue_q = [&](int kt, int slot, int q) {
     char* base = smem + slot * STAGE;
 #pragma unroll
     for (int j = 0; j < A_LOADS; ++j)
-      if (j % 4 == q) load_lds16(pa[j] + kt * BK, base + (wave * A_LOADS + j) * 1024);
+      if (j % KS == q) load_lds16(pa[j] + kt * BK, base + (wave * A_LOADS + j) * 1024);
 #pragma unroll
     for (int j = 0; j < B_LOADS; ++j)
-      if (j % 4 == q) load_lds16(pb[j] + kt * BK, base + A_BYTES + (wave * B_LOADS + j) * 1024);
+      if (j % KS == q) load_lds16(pb[j] + kt * BK, base + A_BYTES + (wave * B_LOADS + j) * 1024);
   };
 
   f32x16 acc[MB][NB];
@@ -213,10 +231,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
     const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
     for (int i = 0; i < MB; ++i)
-      fa[set][i] = *(const bf16x8*)(st + arow[i] * 128 + ((chunk ^ swz(arow[i])) << 4));
+      fa[set][i] = *(const bf16x8*)(st + arow[i] * ROWB + ((chunk ^ swz<BK>(arow[i])) << 4));
 #pragma unroll
     for (int j = 0; j < NB; ++j)
-      fb[set][j] = *(const bf16x8*)(st + A_BYTES + brow[j] * 128 + ((chunk ^ swz(brow[j])) << 4));
+      fb[set][j] = *(const bf16x8*)(st + A_BYTES + brow[j] * ROWB + ((chunk ^ swz<BK>(brow[j])) << 4));
   };
   auto mfmas = [&](int set) {
 #pragma unroll
@@ -231,27 +249,24 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   for (int st = 0; st < NS - 1; ++st)
     if (st < KT) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) issue_q(st, st, q);
+      for (int q = 0; q < KS; ++q) issue_q(st, st, q);
     }
   if (KT >= NS - 1) wait_vm<(NS - 2) * LPW>();
   else wait_vm<0>();
   ring_barrier();
-  // Stage pk (slot ps) is issued quarter by quarter between the MFMA blocks
-  // of the current step; -1 when none is left.
+  // Stage pk (slot ps) is issued part by part between the MFMA blocks of the
+  // current step; -1 when none is left.
   int pk = NS - 1 < KT ? NS - 1 : -1, ps = NS - 1;
   if (pk >= 0) issue_q(pk, ps, 0);
   load_frags(smem, 0, 0);
   for (int kt = 0; kt < KT; ++kt) {
     const char* st = smem + (kt % NS) * STAGE;
-    load_frags(st, 1, 1);
-    if (pk >= 0) issue_q(pk, ps, 1);
-    mfmas(0);
-    load_frags(st, 2, 0);
-    if (pk >= 0) issue_q(pk, ps, 2);
-    mfmas(1);
-    load_frags(st, 3, 1);
-    if (pk >= 0) issue_q(pk, ps, 3);
-    mfmas(0);
+#pragma unroll
+    for (int ks = 0; ks + 1 < KS; ++ks) {
+      load_frags(st, ks + 1, (ks + 1) & 1);
+      if (pk >= 0) issue_q(pk, ps, ks + 1);
+      mfmas(ks & 1);
+    }
     pk = -1;
     if (kt + 1 < KT) {
       // Stage kt+1 has landed for every wave (stages kt+2 .. kt+NS-1 may
@@ -267,7 +282,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
       }
       load_frags(smem + ((kt + 1) % NS) * STAGE, 0, 0);
     }
-    mfmas(1);
+    mfmas((KS - 1) & 1);
   }
 
   // Accumulator layout of a 32x32 block: lane l, element e holds
@@ -391,8 +406,9 @@ enum TileShape { TILE_256x256, TILE_256x128, TILE_128x128_2WG, TILE_128x128, TIL
 //   * up to 128 rows: 128 x 128 tiles with a 4-stage ring (one work-group per
 //     CU, deep lookahead for the weight stream);
 //   * many rows and at least 384 256 x 256 tiles (gate/up, LM head): 256 x 256
-//     tiles, whose 2-stage ring fills the LDS; they need the fewest operand
-//     bytes per flop;
+//     tiles, which need the fewest operand bytes per flop, with 32-wide K
+//     steps in a 4-stage ring (128 KB; 3-5 % faster than 64-wide steps in
+//     two stages);
 //   * the q/k/v projection at 512 rows and more: 128 x 128 tiles with a
 //     2-stage ring, two work-groups per CU, so that one group's epilogue
 //     (rotary, scattered cache writes) overlaps the other's main loop;
@@ -414,7 +430,7 @@ TileShape pick_tile(int epi, int M, int N, int K, int n0, int n1) {
 // K splits: about one work-group per CU for the wide tiles (their ring holds
 // a CU's LDS) and two for the skinny ones, at least 8 K steps per split, the
 // splits dividing the K steps, partials within the workspace area.
-int choose_splits(int epi, int BM, long tiles, int M, int N, int K) {
+int choose_splits(int epi, int BM, int BK, long tiles, int M, int N, int K) {
   if (epi == EPI_ARGMAX) return 1;
   const long target = BM <= 64 ? 512 : 256;
   int s = (int)std::max<long>(1, std::min<long>(16, target / tiles));
@@ -423,19 +439,19 @@ int choose_splits(int epi, int BM, long tiles, int M, int N, int K) {
   return s;
 }
 
-template <int EPI, int BM, int BN, int WM, int NS>
+template <int EPI, int BM, int BN, int WM, int NS, int BK = 64>
 hipError_t launch_tile(GemmArgs a, hipStream_t s) {
   constexpr int SMEM = NS * (BM + BN) * BK * 2;
   static bool configured = false;
   if (!configured) {
-    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN, WM, NS>,
+    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN, WM, NS, BK>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
     if (e != hipSuccess) return e;
     configured = true;
   }
   const long tiles = (long)((a.M + BM - 1) / BM) * (a.N / BN);
-  a.ksplit = a.partial ? choose_splits(EPI, BM, tiles, a.M, a.N, a.K) : 1;
-  gemm_bf16_kernel<EPI, BM, BN, WM, NS><<<(unsigned)(tiles * a.ksplit), NT, SMEM, s>>>(a);
+  a.ksplit = a.partial ? choose_splits(EPI, BM, BK, tiles, a.M, a.N, a.K) : 1;
+  gemm_bf16_kernel<EPI, BM, BN, WM, NS, BK><<<(unsigned)(tiles * a.ksplit), NT, SMEM, s>>>(a);
   if (a.ksplit > 1) {
     const size_t threads = (size_t)a.M * (a.N / 2);
     splitk_reduce_kernel<EPI, BN><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
@@ -446,7 +462,7 @@ hipError_t launch_tile(GemmArgs a, hipStream_t s) {
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
   switch (pick_tile(EPI, a.M, a.N, a.K, a.n0, a.n1)) {
-    case TILE_256x256: return launch_tile<EPI, 256, 256, 2, 2>(a, s);
+    case TILE_256x256: return launch_tile<EPI, 256, 256, 2, 4, 32>(a, s);
     case TILE_256x128: return launch_tile<EPI, 256, 128, 2, 3>(a, s);
     case TILE_128x128_2WG: return launch_tile<EPI, 128, 128, 2, 2>(a, s);
     case TILE_32x256: return launch_tile<EPI, 32, 256, 1, 3>(a, s);
