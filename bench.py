@@ -41,6 +41,9 @@ def parse():
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="only copy BYTES device-to-device 5 times (a reference for the HBM "
                         "byte counters) and exit")
+    p.add_argument("--kv-migrate", action="store_true",
+                   help="time the migration buffer instead: pack + unpack of 16 samples' K/V "
+                        "at the Llama-3-8B shape (lognormal lengths, median 1024)")
     p.add_argument("--sweep", default=None, metavar="OUT.jsonl",
                    help="run the strategy-cost sweep (batch x tree budget) and write one JSON "
                         "line per cell to OUT.jsonl")
@@ -121,6 +124,57 @@ def run_sweep(args, out_path):
     return rows
 
 
+def run_kv_migrate(args):
+    """Sample migration's KV transfer (paper Section 6.2, phases 1 and 3) at the
+    Llama-3-8B shape: 16 samples with lognormal committed lengths (median 1024,
+    sigma 0.8, clipped to [128, 8192], the early-generation distribution) are
+    packed from a source pool into one contiguous buffer and unpacked into a
+    destination pool.  Each kernel moves every byte twice (read + write); the
+    bound is HBM bandwidth."""
+    import torch
+
+    import paper_2512_04752_amd as sv
+    import workload as wl
+
+    cfg = wl.LLAMA_8B
+    rng = np.random.default_rng(6000)
+    lens = [int(x) for x in np.clip(np.round(rng.lognormal(np.log(1024), 0.8, 16)), 128, 8192)]
+    src = sv.KVPool(cfg, lens)
+    dst = sv.KVPool(cfg, [max(lens) + 64] * 16)
+    src.buf.fill_(1)
+    ids = list(range(16))
+    dids = ids[::-1]
+    begin, end = [0] * 16, lens
+    nbytes = sv.spec_kv_transfer_bytes(src, begin, end)
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        sv.spec_kv_pack(src, ids, begin, end, buf, stream=stream)
+        sv.spec_kv_unpack(dst, dids, begin, end, buf, stream=stream)
+    torch.cuda.synchronize()
+    res = {}
+    for name, fn in (("pack", lambda: sv.spec_kv_pack(src, ids, begin, end, buf, stream=stream)),
+                     ("unpack", lambda: sv.spec_kv_unpack(dst, dids, begin, end, buf,
+                                                          stream=stream))):
+        sv.spec_profile_begin("transfer", args.steps + 1)
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        ms, n = sv.spec_profile_end()
+        avg = ms / max(n, 1)
+        gbs = 2 * nbytes / (avg / 1e3) / 1e9
+        res[name] = {"avg_launch_ms": round(avg, 4), "launches": n, "achieved": round(gbs, 1),
+                     "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return {"metric": "KV transfer GB/s (read + write), sample migration phases 1 and 3",
+            "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "config": {"workload": "Llama-3-8B shape, 16 samples, KV lengths lognormal(median "
+                                   "1024, sigma 0.8) in [128, 8192]", "tokens": int(sum(lens)),
+                       "buffer_bytes": int(nbytes)},
+            "dtype": "bf16 (bytes copied)", "roofline": {"bound": "hbm", "peak": PEAK_HBM_GBS,
+                                                          "unit": "GB/s", "pack": res["pack"],
+                                                          "unpack": res["unpack"]}}
+
+
 def recorded_traffic(workload, kernel):
     """HBM bytes per launch of `kernel` on `workload` from the committed
     copy-calibrated rocprofv3 counter summary, or None when there is none or
@@ -199,6 +253,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": args.copy_calibration, "copies": 5}), flush=True)
+        return
+    if args.kv_migrate:
+        print(json.dumps(run_kv_migrate(args)), flush=True)
         return
     if args.sweep:
         rows = run_sweep(args, args.sweep)

@@ -166,6 +166,44 @@ int spec_kv_commit(spec_kv* kv, int32_t batch, const int32_t* sample_ids,
                    const int32_t* seq_lens, const int32_t* accepted_len,
                    const int32_t* accepted_nodes, int32_t* new_seq_lens, void* stream);
 
+/* ---- KV transfer for sample migration ----------------------------------
+ * (Section 6.2, "Two-stage Sample Migration": phase 1 copies the K/V of the
+ * migrating samples out of the cache store into one contiguous buffer, so
+ * that the transfer is a single copy; phase 3 parses such a buffer and
+ * appends its K/V to the destination store.  Verified K/V never changes
+ * (the Markov property the paper relies on), so stage 1 can move the
+ * verified prefix [0, S) while the sample keeps running and stage 2 only the
+ * tokens verified since: both are a token range [begin, end) per sample.)
+ *
+ * Buffer layout, the paper's model -> layer -> sample order (this library
+ * holds one model, the LLM):
+ *   [layer][K=0,V=1][sample j in call order][kv_head][token begin_j .. end_j-1][head_dim]
+ * bf16, no padding; its size is spec_kv_transfer_bytes.
+ *
+ *   sample_ids host [n]  distinct pool samples, 1 <= n <= pool samples
+ *   tok_begin  host [n]  first token of each range, 0 <= begin
+ *   tok_end    host [n]  one past the last, begin <= end <= capacity
+ *                        (empty ranges are allowed and contribute nothing)
+ *   buf        device, 16-byte aligned, buf_bytes >= spec_kv_transfer_bytes
+ * The buffer belongs to the caller.  Returns SPEC_ERR_CAPACITY for a range
+ * outside a sample's capacity or a buffer that is too small; nothing is
+ * enqueued then. */
+
+/* Bytes of the transfer buffer for these ranges (0 if an argument is invalid). */
+size_t spec_kv_transfer_bytes(const spec_kv* kv, int32_t n, const int32_t* tok_begin,
+                              const int32_t* tok_end);
+
+/* Phase 1: copy positions [begin_j, end_j) of every layer, K and V and KV
+ * head of sample sample_ids[j] into buf.  Reads the pool only. */
+int spec_kv_pack(spec_kv* kv, int32_t n, const int32_t* sample_ids, const int32_t* tok_begin,
+                 const int32_t* tok_end, void* buf, size_t buf_bytes, void* stream);
+
+/* Phase 3: the reverse: write buf's runs to positions [begin_j, end_j) of
+ * sample sample_ids[j] of this pool (the destination of the migration; the
+ * caller raises its committed lengths afterwards).  Reads buf only. */
+int spec_kv_unpack(spec_kv* kv, int32_t n, const int32_t* sample_ids, const int32_t* tok_begin,
+                   const int32_t* tok_end, const void* buf, size_t buf_bytes, void* stream);
+
 /* Message of the last failure on the calling thread ("" if none). */
 const char* spec_last_error(void);
 
@@ -182,7 +220,8 @@ enum {
   SPEC_K_GEMM_DOWN = 4,
   SPEC_K_LM_HEAD = 5,
   SPEC_K_COMMIT = 6,
-  SPEC_K_COUNT = 7
+  SPEC_K_TRANSFER = 7,   /* spec_kv_pack / spec_kv_unpack */
+  SPEC_K_COUNT = 8
 };
 int spec_profile_begin(int32_t kernel_class, int32_t max_launches);
 int spec_profile_end(float* total_ms, int32_t* launches);

@@ -16,7 +16,10 @@ from .binding import (  # noqa: F401
     spec_kv_bytes,
     spec_kv_commit,
     spec_kv_free,
+    spec_kv_pack,
     spec_kv_sample_layout,
+    spec_kv_transfer_bytes,
+    spec_kv_unpack,
     spec_profile_begin,
     spec_profile_end,
     spec_verify,

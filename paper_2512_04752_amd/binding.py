@@ -19,12 +19,14 @@ SPEC_MAX_TREE = 64
 STATUS = {0: "SPEC_OK", -1: "SPEC_ERR_INVALID", -2: "SPEC_ERR_TREE", -3: "SPEC_ERR_CAPACITY",
           -5: "SPEC_ERR_WORKSPACE", -6: "SPEC_ERR_UNSUPPORTED", -7: "SPEC_ERR_HIP"}
 KERNEL_CLASS = {"gemm_qkv": 0, "attention": 1, "gemm_o": 2, "gemm_gate_up": 3, "gemm_down": 4,
-                "lm_head": 5, "commit": 6}
+                "lm_head": 5, "commit": 6}          # the kernel classes of one verify step
+TRANSFER_CLASS = 7                                    # spec_kv_pack / spec_kv_unpack
 
 # Every symbol the public header declares.
 EXPORTS = ("spec_kv_bytes", "spec_kv_alloc", "spec_kv_free", "spec_kv_sample_layout",
            "spec_workspace_bytes", "spec_verify", "spec_kv_commit", "spec_last_error",
-           "spec_profile_begin", "spec_profile_end")
+           "spec_profile_begin", "spec_profile_end", "spec_kv_transfer_bytes", "spec_kv_pack",
+           "spec_kv_unpack")
 
 
 class SpecError(RuntimeError):
@@ -78,11 +80,16 @@ def lib():
                               c_void_p, c_void_p, c_void_p, c_void_p, POINTER(spec_debug)]
     L.spec_kv_commit.argtypes = [c_void_p, c_int32, i32p, i32p, c_void_p, c_void_p, c_void_p,
                                  c_void_p]
+    L.spec_kv_transfer_bytes.argtypes = [c_void_p, c_int32, i32p, i32p]
+    L.spec_kv_transfer_bytes.restype = c_size_t
+    L.spec_kv_pack.argtypes = [c_void_p, c_int32, i32p, i32p, i32p, c_void_p, c_size_t, c_void_p]
+    L.spec_kv_unpack.argtypes = [c_void_p, c_int32, i32p, i32p, i32p, c_void_p, c_size_t, c_void_p]
     L.spec_last_error.restype = ctypes.c_char_p
     L.spec_profile_begin.argtypes = [c_int32, c_int32]
     L.spec_profile_end.argtypes = [POINTER(c_float), i32p]
     for name in ("spec_kv_alloc", "spec_kv_free", "spec_kv_sample_layout", "spec_verify",
-                 "spec_kv_commit", "spec_profile_begin", "spec_profile_end"):
+                 "spec_kv_commit", "spec_profile_begin", "spec_profile_end", "spec_kv_pack",
+                 "spec_kv_unpack"):
         getattr(L, name).restype = c_int32
     _lib = L
     return L
@@ -230,8 +237,36 @@ def spec_kv_commit(kv: KVPool, sample_ids, seq_lens, accepted_len, accepted_node
                                 _ptr(accepted_nodes), _ptr(new_seq_lens), _stream(stream)))
 
 
+def spec_kv_transfer_bytes(kv: KVPool, tok_begin, tok_end) -> int:
+    b, p_b = _i32(tok_begin)
+    e, p_e = _i32(tok_end)
+    return int(lib().spec_kv_transfer_bytes(kv.handle, len(b), p_b, p_e))
+
+
+def spec_kv_pack(kv: KVPool, sample_ids, tok_begin, tok_end, buf, stream=None):
+    """Copy token ranges of the given samples into the transfer buffer ``buf``
+    (a device tensor of at least spec_kv_transfer_bytes bytes)."""
+    ids, p_ids = _i32(sample_ids)
+    b, p_b = _i32(tok_begin)
+    e, p_e = _i32(tok_end)
+    _check(lib().spec_kv_pack(kv.handle, len(ids), p_ids, p_b, p_e, _ptr(buf),
+                              buf.numel() * buf.element_size(), _stream(stream)))
+
+
+def spec_kv_unpack(kv: KVPool, sample_ids, tok_begin, tok_end, buf, stream=None):
+    """Write a transfer buffer's runs into token ranges of this pool's samples."""
+    ids, p_ids = _i32(sample_ids)
+    b, p_b = _i32(tok_begin)
+    e, p_e = _i32(tok_end)
+    _check(lib().spec_kv_unpack(kv.handle, len(ids), p_ids, p_b, p_e, _ptr(buf),
+                                buf.numel() * buf.element_size(), _stream(stream)))
+
+
 def spec_profile_begin(kernel_class, max_launches):
-    k = KERNEL_CLASS[kernel_class] if isinstance(kernel_class, str) else int(kernel_class)
+    if kernel_class == "transfer":
+        k = TRANSFER_CLASS
+    else:
+        k = KERNEL_CLASS[kernel_class] if isinstance(kernel_class, str) else int(kernel_class)
     _check(lib().spec_profile_begin(k, max_launches))
 
 

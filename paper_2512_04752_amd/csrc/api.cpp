@@ -604,6 +604,88 @@ SPEC_API int spec_kv_commit(spec_kv* kv, int32_t batch, const int32_t* sample_id
   return SPEC_OK;
 }
 
+namespace {
+
+// Validate a transfer request and build its per-sample descriptors.
+int transfer_plan(const spec_kv* kv, int32_t n, const int32_t* sample_ids, const int32_t* tok_begin,
+                  const int32_t* tok_end, std::vector<MigrateInfo>* info, int64_t* wg_per_slab,
+                  int64_t* tok_total) {
+  if (!kv || !sample_ids || !tok_begin || !tok_end) return fail(SPEC_ERR_INVALID, "null argument");
+  if (n < 1 || n > kv->n) return fail(SPEC_ERR_INVALID, "n %d out of range", n);
+  if (int rc = check_samples(kv, n, sample_ids)) return rc;
+  const spec_model_config& c = kv->cfg;
+  info->resize(n);
+  int64_t wg = 0, tok = 0;
+  for (int j = 0; j < n; ++j) {
+    const int id = sample_ids[j];
+    if (tok_begin[j] < 0 || tok_end[j] < tok_begin[j] || tok_end[j] > kv->cap[id])
+      return fail(SPEC_ERR_CAPACITY, "token range [%d, %d) of sample %d outside capacity %d",
+                  tok_begin[j], tok_end[j], id, kv->cap[id]);
+    const int count = tok_end[j] - tok_begin[j];
+    const int64_t chunks = kv_transfer_chunks(count, c.head_dim);
+    (*info)[j] = MigrateInfo{kv->base[id], kv->cap[id], tok_begin[j], count, (int32_t)tok,
+                             (int32_t)wg, (int32_t)chunks};
+    wg += chunks * c.n_kv_heads;
+    tok += count;
+    if (wg > 0x7fffffff || tok > 0x7fffffff) return fail(SPEC_ERR_INVALID, "transfer too large");
+  }
+  *wg_per_slab = wg;
+  *tok_total = tok;
+  return SPEC_OK;
+}
+
+int transfer(bool to_buffer, spec_kv* kv, int32_t n, const int32_t* sample_ids,
+             const int32_t* tok_begin, const int32_t* tok_end, void* buf, size_t buf_bytes,
+             void* stream) {
+  g_err.clear();
+  std::vector<MigrateInfo> info;
+  int64_t wg = 0, tok = 0;
+  if (int rc = transfer_plan(kv, n, sample_ids, tok_begin, tok_end, &info, &wg, &tok)) return rc;
+  if (!buf) return fail(SPEC_ERR_INVALID, "null buffer");
+  if ((uintptr_t)buf % 16) return fail(SPEC_ERR_INVALID, "buffer not 16-byte aligned");
+  const spec_model_config& c = kv->cfg;
+  const size_t need = (size_t)tok * c.n_layers * 2 * c.n_kv_heads * c.head_dim * 2;
+  if (buf_bytes < need)
+    return fail(SPEC_ERR_CAPACITY, "transfer buffer holds %zu bytes, needs %zu", buf_bytes, need);
+  if (wg == 0) return SPEC_OK;
+  hipStream_t s = (hipStream_t)stream;
+  void* ctl = (char*)kv->pool + kv->ctl_off;
+  if (int rc = stage_upload(kv, info.data(), n * sizeof(MigrateInfo), ctl, s)) return rc;
+  HIP_TRY(timed(SPEC_K_TRANSFER, s, [&] {
+            return launch_kv_transfer(to_buffer, (const MigrateInfo*)ctl, n, wg, (int)tok, kv->pool,
+                                      (bf16*)buf, c.n_layers, c.n_kv_heads, c.head_dim, s);
+          }),
+          to_buffer ? "kv pack" : "kv unpack");
+  return SPEC_OK;
+}
+
+}  // namespace
+
+SPEC_API size_t spec_kv_transfer_bytes(const spec_kv* kv, int32_t n, const int32_t* tok_begin,
+                                       const int32_t* tok_end) {
+  if (!kv || !tok_begin || !tok_end || n < 1) return 0;
+  size_t tok = 0;
+  for (int j = 0; j < n; ++j) {
+    if (tok_end[j] < tok_begin[j] || tok_begin[j] < 0) return 0;
+    tok += (size_t)(tok_end[j] - tok_begin[j]);
+  }
+  const spec_model_config& c = kv->cfg;
+  return tok * c.n_layers * 2 * c.n_kv_heads * c.head_dim * 2;
+}
+
+SPEC_API int spec_kv_pack(spec_kv* kv, int32_t n, const int32_t* sample_ids,
+                          const int32_t* tok_begin, const int32_t* tok_end, void* buf,
+                          size_t buf_bytes, void* stream) {
+  return transfer(true, kv, n, sample_ids, tok_begin, tok_end, buf, buf_bytes, stream);
+}
+
+SPEC_API int spec_kv_unpack(spec_kv* kv, int32_t n, const int32_t* sample_ids,
+                            const int32_t* tok_begin, const int32_t* tok_end, const void* buf,
+                            size_t buf_bytes, void* stream) {
+  return transfer(false, kv, n, sample_ids, tok_begin, tok_end, const_cast<void*>(buf), buf_bytes,
+                  stream);
+}
+
 SPEC_API int spec_profile_begin(int32_t kernel_class, int32_t max_launches) {
   if (kernel_class < 0 || kernel_class >= SPEC_K_COUNT || max_launches < 1)
     return fail(SPEC_ERR_INVALID, "bad profile request");

@@ -46,6 +46,18 @@ struct AttnItem {
 };
 static_assert(sizeof(AttnItem) == 32, "AttnItem layout");
 
+// One sample of a KV transfer (pack or unpack of a token range).
+struct MigrateInfo {
+  int64_t kv_base;      // element offset of the sample's block in the KV pool
+  int32_t cap;          // positions per (layer, K/V, kv head)
+  int32_t begin;        // first token of the range
+  int32_t count;        // tokens in the range
+  int32_t tok_prefix;   // tokens of the samples before this one in the call
+  int32_t wg_prefix;    // work-groups of the samples before it, within one (layer, K/V)
+  int32_t chunks;       // work-groups per (layer, K/V, kv head) run of this sample
+};
+static_assert(sizeof(MigrateInfo) == 32, "MigrateInfo layout");
+
 // One split-combine job: nsplit partial tiles starting at slot part0.
 struct CombineItem {
   int32_t sample, kvh, row0, nsplit, part0, pad0, pad1, pad2;
@@ -130,6 +142,14 @@ hipError_t launch_accept(const SampleInfo* samples, int batch, const int32_t* to
                          const int32_t* parents, const TokInfo* toks, const int32_t* argmax,
                          int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
                          hipStream_t s);
+// Work-groups one (layer, K/V, kv head) run of `count` tokens takes.
+int64_t kv_transfer_chunks(int count, int head_dim);
+// Copy the runs described by info[0..n) between the pool and the transfer
+// buffer (to_buffer: pool -> buffer, else buffer -> pool); wg_per_slab =
+// sum over samples of n_kv_heads * chunks, tok_total = sum of counts.
+hipError_t launch_kv_transfer(bool to_buffer, const MigrateInfo* info, int n, int64_t wg_per_slab,
+                              int tok_total, bf16* pool, bf16* buf, int n_layers, int n_kv_heads,
+                              int head_dim, hipStream_t s);
 hipError_t launch_compact(const SampleInfo* samples, int batch, bf16* kv_pool, int n_layers,
                           int n_kv_heads, int head_dim, const int32_t* accepted_len,
                           const int32_t* accepted_nodes, int32_t* new_seq_lens, hipStream_t s);

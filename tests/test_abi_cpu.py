@@ -196,3 +196,32 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         B.lib()
+
+
+def test_transfer_bytes_and_validation(fake):
+    """spec_kv_transfer_bytes arithmetic and the pack/unpack rejections, all
+    before any device work (fake device pointers are never touched)."""
+    L = fake.L
+    cfg = fake.cfg
+    i32 = lambda *v: (ctypes.c_int32 * len(v))(*v)
+    per_tok = cfg.n_layers * 2 * cfg.n_kv_heads * cfg.head_dim * 2
+    assert L.spec_kv_transfer_bytes(fake.kv, 2, i32(3, 0), i32(10, 0)) == 7 * per_tok
+    assert L.spec_kv_transfer_bytes(fake.kv, 2, i32(3, 5), i32(10, 4)) == 0      # end < begin
+    need = 12 * per_tok
+    buf = ctypes.c_void_p(FAKE_DEV)
+    for fn in (L.spec_kv_pack, L.spec_kv_unpack):
+        # range past the capacity (200)
+        assert fn(fake.kv, 2, i32(0, 1), i32(0, 195), i32(10, 202), buf, need, None) == -3
+        # buffer too small
+        assert fn(fake.kv, 2, i32(0, 1), i32(0, 0), i32(5, 7), buf, need - 1, None) == -3
+        # misaligned buffer
+        assert fn(fake.kv, 1, i32(0), i32(0), i32(5), ctypes.c_void_p(FAKE_DEV + 8), need,
+                  None) == -1
+        # duplicate and out-of-range sample ids
+        assert fn(fake.kv, 2, i32(1, 1), i32(0, 0), i32(1, 1), buf, need, None) == -1
+        assert fn(fake.kv, 1, i32(3), i32(0), i32(1), buf, need, None) == -1
+        # negative begin
+        assert fn(fake.kv, 1, i32(0), i32(-1), i32(1), buf, need, None) == -3
+        assert L.spec_last_error()
+    # nothing to move: accepted without device work
+    assert L.spec_kv_pack(fake.kv, 1, i32(0), i32(4), i32(4), buf, 0, None) == 0
