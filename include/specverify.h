@@ -204,6 +204,57 @@ int spec_kv_pack(spec_kv* kv, int32_t n, const int32_t* sample_ids, const int32_
 int spec_kv_unpack(spec_kv* kv, int32_t n, const int32_t* sample_ids, const int32_t* tok_begin,
                    const int32_t* tok_end, const void* buf, size_t buf_bytes, void* stream);
 
+/* ---- Drafting-strategy selection (Section 5) ----------------------------
+ *
+ * Verification-cost predictor (Section 5.2, "the execution time"): a
+ * regression on the verification features, in milliseconds,
+ *   t_sd = c0 + c_seq * N_seq + c_draft * N_draft + c_tree * TK
+ * with N_seq = sum of committed lengths S_b (the KV the attention loads),
+ * N_draft = sum of tree sizes T_b (the rows of the FFN products) and
+ * TK = sum of T_b * S_b (the attention work that grows with both).  The
+ * coefficients are fitted offline on measured steps of this library.
+ * Bucket cache: with bucket_ratio r > 0, every feature x > 0 falls in bucket
+ * floor(log(x) / log(1 + r)) (0 has its own bucket); all feature triples in
+ * one bucket share the prediction at the buckets' geometric midpoints, which
+ * is computed once and then read from the cache.  r = 0 disables it. */
+typedef struct {
+  double c0, c_seq, c_draft, c_tree;
+  double bucket_ratio;
+} spec_cost_coeffs;
+
+typedef struct spec_cost_model spec_cost_model;   /* opaque, host, owned by the library */
+
+int spec_cost_model_create(const spec_cost_coeffs* coeffs, spec_cost_model** out);
+int spec_cost_model_free(spec_cost_model* model);
+/* Predicted step time in ms, or a negative value for a negative feature. */
+double spec_cost_predict(spec_cost_model* model, int64_t n_seq, int64_t n_draft, int64_t tree_kv);
+/* Cache hits and misses since creation. */
+int spec_cost_model_stats(const spec_cost_model* model, int64_t* hits, int64_t* misses);
+
+/* Choose the draft token num n (tree nodes per sample, root included) of the
+ * next step for a batch (Sections 5.1 and 5.3): n maximises
+ * al(n) / t_sd(n), where al(n) = sum over samples of the weights of S_b(n)
+ * and t_sd is the predictor above at the features of trees of min(n, |tree|)
+ * nodes.  S_b(1) = {root}; S_b(n+1) adds the heaviest unselected node of the
+ * sample's candidate tree, taken from a max-priority queue that receives the
+ * nodes of layer m (depth m) when the search reaches layer m; equal weights
+ * go to the shallower node, then the lower index.  Since weights never grow
+ * from parent to child, S_b(n) is a connected tree.  The search over n stops
+ * after `patience` consecutive falls of the objective.
+ *   seq_lens      host [batch]    committed length S_b of each sample
+ *   tree_offsets  host [batch+1]  candidate trees, offsets[0] = 0, sizes >= 1
+ *   parents       host [total]    parent within the tree, -1 for node 0,
+ *                                 0 <= parent < node otherwise
+ *   weights       host [total]    w(u) = F(dl(u)) >= 0, w(child) <= w(parent)
+ *   n_max         1 .. SPEC_MAX_TREE
+ * Outputs (host): *n_out; selected [batch][n_max], sample b's nodes in the
+ * order they joined S_b (the first n form S_b(n)), -1 past the tree's size;
+ * objective [n_max] (may be NULL): al(n) / t_sd(n), 0 past the stop. */
+int spec_select_draft_count(spec_cost_model* model, int32_t batch, const int32_t* seq_lens,
+                            const int32_t* tree_offsets, const int32_t* parents,
+                            const float* weights, int32_t n_max, int32_t patience, int32_t* n_out,
+                            int32_t* selected, double* objective);
+
 /* Message of the last failure on the calling thread ("" if none). */
 const char* spec_last_error(void);
 

@@ -7,6 +7,7 @@ loaded on first use and its absence is an error.
 
 from .binding import (  # noqa: F401
     EXPORTS,
+    CostModel,
     KVPool,
     SPEC_MAX_TREE,
     SpecError,
@@ -22,6 +23,7 @@ from .binding import (  # noqa: F401
     spec_kv_unpack,
     spec_profile_begin,
     spec_profile_end,
+    spec_select_draft_count,
     spec_verify,
     spec_workspace_bytes,
 )

@@ -26,7 +26,8 @@ TRANSFER_CLASS = 7                                    # spec_kv_pack / spec_kv_u
 EXPORTS = ("spec_kv_bytes", "spec_kv_alloc", "spec_kv_free", "spec_kv_sample_layout",
            "spec_workspace_bytes", "spec_verify", "spec_kv_commit", "spec_last_error",
            "spec_profile_begin", "spec_profile_end", "spec_kv_transfer_bytes", "spec_kv_pack",
-           "spec_kv_unpack")
+           "spec_kv_unpack", "spec_cost_model_create", "spec_cost_model_free", "spec_cost_predict",
+           "spec_cost_model_stats", "spec_select_draft_count")
 
 
 class SpecError(RuntimeError):
@@ -47,6 +48,11 @@ class spec_weights(ctypes.Structure):
                 ("wk", POINTER(c_void_p)), ("wv", POINTER(c_void_p)), ("wo", POINTER(c_void_p)),
                 ("ffn_norm", POINTER(c_void_p)), ("w_gate", POINTER(c_void_p)),
                 ("w_up", POINTER(c_void_p)), ("w_down", POINTER(c_void_p))]
+
+
+class spec_cost_coeffs(ctypes.Structure):
+    _fields_ = [("c0", ctypes.c_double), ("c_seq", ctypes.c_double), ("c_draft", ctypes.c_double),
+                ("c_tree", ctypes.c_double), ("bucket_ratio", ctypes.c_double)]
 
 
 class spec_debug(ctypes.Structure):
@@ -84,12 +90,21 @@ def lib():
     L.spec_kv_transfer_bytes.restype = c_size_t
     L.spec_kv_pack.argtypes = [c_void_p, c_int32, i32p, i32p, i32p, c_void_p, c_size_t, c_void_p]
     L.spec_kv_unpack.argtypes = [c_void_p, c_int32, i32p, i32p, i32p, c_void_p, c_size_t, c_void_p]
+    L.spec_cost_model_create.argtypes = [POINTER(spec_cost_coeffs), POINTER(c_void_p)]
+    L.spec_cost_model_free.argtypes = [c_void_p]
+    L.spec_cost_predict.argtypes = [c_void_p, c_int64, c_int64, c_int64]
+    L.spec_cost_predict.restype = ctypes.c_double
+    L.spec_cost_model_stats.argtypes = [c_void_p, POINTER(c_int64), POINTER(c_int64)]
+    L.spec_select_draft_count.argtypes = [c_void_p, c_int32, i32p, i32p, i32p,
+                                          POINTER(c_float), c_int32, c_int32, i32p, i32p,
+                                          POINTER(ctypes.c_double)]
     L.spec_last_error.restype = ctypes.c_char_p
     L.spec_profile_begin.argtypes = [c_int32, c_int32]
     L.spec_profile_end.argtypes = [POINTER(c_float), i32p]
     for name in ("spec_kv_alloc", "spec_kv_free", "spec_kv_sample_layout", "spec_verify",
                  "spec_kv_commit", "spec_profile_begin", "spec_profile_end", "spec_kv_pack",
-                 "spec_kv_unpack"):
+                 "spec_kv_unpack", "spec_cost_model_create", "spec_cost_model_free",
+                 "spec_cost_model_stats", "spec_select_draft_count"):
         getattr(L, name).restype = c_int32
     _lib = L
     return L
@@ -260,6 +275,60 @@ def spec_kv_unpack(kv: KVPool, sample_ids, tok_begin, tok_end, buf, stream=None)
     e, p_e = _i32(tok_end)
     _check(lib().spec_kv_unpack(kv.handle, len(ids), p_ids, p_b, p_e, _ptr(buf),
                                 buf.numel() * buf.element_size(), _stream(stream)))
+
+
+class CostModel:
+    """The library's verification-cost predictor (spec_cost_model_*)."""
+
+    def __init__(self, c0, c_seq, c_draft, c_tree, bucket_ratio=0.0):
+        self.coeffs = spec_cost_coeffs(c0, c_seq, c_draft, c_tree, bucket_ratio)
+        h = c_void_p()
+        _check(lib().spec_cost_model_create(ctypes.byref(self.coeffs), ctypes.byref(h)))
+        self.handle = h
+
+    @classmethod
+    def from_dict(cls, d, bucket_ratio=None):
+        return cls(d["c0"], d["c_seq"], d["c_draft"], d["c_tree"],
+                   d.get("bucket_ratio", 0.0) if bucket_ratio is None else bucket_ratio)
+
+    def predict(self, n_seq, n_draft, tree_kv):
+        t = lib().spec_cost_predict(self.handle, int(n_seq), int(n_draft), int(tree_kv))
+        if t < 0:
+            raise SpecError(-1, "negative feature")
+        return t
+
+    def stats(self):
+        h, m = c_int64(), c_int64()
+        _check(lib().spec_cost_model_stats(self.handle, ctypes.byref(h), ctypes.byref(m)))
+        return h.value, m.value
+
+    def close(self):
+        if self.handle is not None:
+            _check(lib().spec_cost_model_free(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def spec_select_draft_count(model: CostModel, seq_lens, tree_offsets, parents, weights, n_max,
+                            patience=2):
+    """Returns (n, selected [batch][n_max] int32 array, objective [n_max])."""
+    lens, p_lens = _i32(seq_lens)
+    offs, p_offs = _i32(tree_offsets)
+    pars, p_pars = _i32(parents)
+    w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    sel = np.empty((len(lens), n_max), dtype=np.int32)
+    obj = np.empty(n_max, dtype=np.float64)
+    n = c_int32()
+    _check(lib().spec_select_draft_count(model.handle, len(lens), p_lens, p_offs, p_pars,
+                                         w.ctypes.data_as(POINTER(c_float)), n_max, patience,
+                                         ctypes.byref(n), sel.ctypes.data_as(POINTER(c_int32)),
+                                         obj.ctypes.data_as(POINTER(ctypes.c_double))))
+    return n.value, sel, obj
 
 
 def spec_profile_begin(kernel_class, max_launches):

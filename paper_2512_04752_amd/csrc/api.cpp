@@ -211,6 +211,13 @@ int check_samples(const spec_kv* kv, int32_t batch, const int32_t* ids) {
 
 SPEC_API const char* spec_last_error(void) { return g_err.c_str(); }
 
+namespace spec {
+int set_error(int code, const char* msg) {
+  g_err = msg;
+  return code;
+}
+}  // namespace spec
+
 SPEC_API size_t spec_kv_bytes(const spec_model_config* cfg, int32_t n_samples,
                               const int32_t* capacity) {
   std::string why;

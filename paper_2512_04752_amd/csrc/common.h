@@ -63,6 +63,9 @@ struct CombineItem {
   int32_t sample, kvh, row0, nsplit, part0, pad0, pad1, pad2;
 };
 
+// Record `msg` as the calling thread's spec_last_error() and return `code`.
+int set_error(int code, const char* msg);
+
 // ---------------------------------------------------------------------------
 // Launchers (each returns hipGetLastError() of its launch)
 // ---------------------------------------------------------------------------
