@@ -44,6 +44,10 @@ def parse():
     p.add_argument("--kv-migrate", action="store_true",
                    help="time the migration buffer instead: pack + unpack of 16 samples' K/V "
                         "at the Llama-3-8B shape (lognormal lengths, median 1024)")
+    p.add_argument("--trajectory", default=None, metavar="OUT.jsonl",
+                   help="run the RLHF generation trajectory (shrinking batch) once per drafting "
+                        "strategy (fixed draft token num, or the workload-aware selection) and "
+                        "write one JSON line per step to OUT.jsonl")
     p.add_argument("--sweep", default=None, metavar="OUT.jsonl",
                    help="run the strategy-cost sweep (batch x tree budget) and write one JSON "
                         "line per cell to OUT.jsonl")
@@ -175,6 +179,146 @@ def run_kv_migrate(args):
                                                           "unpack": res["unpack"]}}
 
 
+def run_trajectory(args, out_path):
+    """Generation stage of one RLHF iteration on one instance, with each
+    drafting strategy (paper Sections 5 and 7.3): 128 samples at the
+    Llama-3-8B shape, prompts with the early-generation length distribution
+    (lognormal, median 1024, sigma 0.8, clipped to [128, 8192]) and response
+    lengths lognormal(median 378, sigma 0.784) clipped to [1, 2048] (the
+    paper's LMSYS response statistics: median 378, 95th percentile 1373).
+    A sample leaves the batch once it has generated its response.
+
+    Every step: each live sample gets a candidate draft tree (top-64 nodes by
+    draft logit of a depth-8, 4-ary tree with Dirichlet(1) sibling scores;
+    node weight w = F(dl) with a linear F of slope 1); the strategy picks the
+    draft token num n (fixed, or spec_select_draft_count with the cost model
+    fitted on this GPU); the top-n nodes are verified by spec_verify (real
+    kernels, random draft tokens); the accepted branch is then drawn from the
+    same acceptance model the selector assumes (child c of an accepted node u
+    is accepted with probability w(c) / w(u), siblings exclusive), and
+    spec_kv_commit compacts it.  Time per step: host selection and tree
+    building + verify + commit, synchronised."""
+    import torch
+
+    import paper_2512_04752_amd as sv
+    import workload as wl
+
+    cfg = wl.LLAMA_8B
+    B0 = 128
+    rng = np.random.default_rng(7000)
+    prompts = [int(x) for x in wl.lognormal_lengths(rng, B0, 1024, 0.8, 128, 8192)]
+    resp = [int(x) for x in np.clip(np.round(rng.lognormal(np.log(378), 0.784, B0)), 1, 2048)]
+    pool_trees = []
+    for _ in range(512):
+        par, dl = wl.draft_logit_tree(rng, 64)
+        pool_trees.append((par, [float(x) for x in dl]))
+    caps = [p + r + 80 for p, r in zip(prompts, resp)]
+    W = wl.make_weights(cfg, 7000, device="cuda")
+    ver = sv.Verifier(cfg, W, caps, max_batch=B0, max_tokens=B0 * 64)
+    data_dir = os.path.join(ROOT, "paper_2512_04752_amd", "data")
+    coeffs = json.load(open(os.path.join(data_dir, "verify_cost_model__llama8b_mi355x.json")))
+    model = sv.CostModel.from_dict(coeffs)
+    stream = torch.cuda.current_stream()
+    strategies = [("fixed", n) for n in (1, 4, 8, 16, 32)] + [("adaptive", 64)]
+    summary = []
+    with open(out_path, "w") as fout:
+        for kind, nmax in strategies:
+            gen = torch.Generator(device="cuda").manual_seed(7000)
+            for b, S in enumerate(prompts):
+                k, v = ver.kv.sample_view(b)
+                wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+            torch.cuda.synchronize()
+            r_step = np.random.default_rng(7001)
+            live = list(range(B0))
+            S_len = list(prompts)
+            done = [0] * B0
+            steps, t_total, t_gpu, tokens, n_sum = 0, 0.0, 0.0, 0, 0
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            while live:
+                t0 = time.perf_counter()
+                picks = r_step.integers(0, len(pool_trees), len(live))
+                trees = [pool_trees[i] for i in picks]
+                offs = np.zeros(len(live) + 1, dtype=np.int32)
+                offs[1:] = np.cumsum([len(t[0]) for t in trees])
+                pars = np.fromiter((x for t in trees for x in t[0]), dtype=np.int32)
+                ws = np.fromiter((x for t in trees for x in t[1]), dtype=np.float32)
+                lens = [S_len[b] for b in live]
+                n_sel, order, _ = sv.spec_select_draft_count(model, lens, offs, pars, ws,
+                                                             nmax if kind == "adaptive" else nmax,
+                                                             patience=2)
+                n = n_sel if kind == "adaptive" else nmax
+                vtrees, vweights = [], []
+                for j, (par, w) in enumerate(trees):
+                    ids = [int(x) for x in order[j, :n] if x >= 0]
+                    pos = {u: k for k, u in enumerate(ids)}
+                    vpar = [-1] + [pos[par[u]] for u in ids[1:]]
+                    vtrees.append((wl.random_tokens(r_step, len(ids), cfg.vocab), vpar))
+                    vweights.append([w[u] for u in ids])
+                # acceptance drawn from the weights (the selector's own model)
+                acc_len = np.zeros(len(live), dtype=np.int32)
+                acc_nodes = np.full((len(live), sv.SPEC_MAX_TREE), -1, dtype=np.int32)
+                for j, ((tok, vpar), w) in enumerate(zip(vtrees, vweights)):
+                    kids = [[] for _ in vpar]
+                    for k in range(1, len(vpar)):
+                        kids[vpar[k]].append(k)
+                    u, path = 0, [0]
+                    while kids[u]:
+                        x = r_step.random() * w[u]
+                        nxt = -1
+                        for c in kids[u]:
+                            if x < w[c]:
+                                nxt = c
+                                break
+                            x -= w[c]
+                        if nxt < 0:
+                            break
+                        u = nxt
+                        path.append(u)
+                    acc_len[j] = len(path) - 1
+                    acc_nodes[j, :len(path)] = path
+                ev0.record(stream)
+                ver.verify(live, vtrees, lens, stream=stream)
+                ver.accepted_len[:len(live)].copy_(torch.from_numpy(acc_len), non_blocking=False)
+                ver.accepted_nodes[:len(live)].copy_(torch.from_numpy(acc_nodes), non_blocking=False)
+                ver.commit(live, lens, stream=stream)
+                ev1.record(stream)
+                torch.cuda.synchronize()
+                t1 = time.perf_counter()
+                dt_gpu = ev0.elapsed_time(ev1)
+                gained = 0
+                still = []
+                for j, b in enumerate(live):
+                    g = int(acc_len[j]) + 1
+                    S_len[b] += g
+                    done[b] += g
+                    gained += g
+                    if done[b] < resp[b]:
+                        still.append(b)
+                fout.write(json.dumps({"strategy": f"{kind}_{nmax}", "step": steps, "batch": len(live),
+                                       "n": int(n), "ms": round((t1 - t0) * 1e3, 3),
+                                       "gpu_ms": round(dt_gpu, 3), "tokens": gained}) + "\n")
+                steps += 1
+                t_total += t1 - t0
+                t_gpu += dt_gpu / 1e3
+                tokens += gained
+                n_sum += n
+                live = still
+            row = {"strategy": kind if kind == "adaptive" else f"fixed n={nmax}", "steps": steps,
+                   "tokens": tokens, "seconds": round(t_total, 3),
+                   "tokens_per_s": round(tokens / t_total, 1),
+                   "gpu_tokens_per_s": round(tokens / t_gpu, 1), "mean_n": round(n_sum / steps, 2)}
+            summary.append(row)
+            print(json.dumps(row), file=sys.stderr, flush=True)
+    hits, misses = model.stats()
+    return {"metric": "RLHF generation trajectory: generated tokens/s per drafting strategy",
+            "unit": "tokens/s", "n_gpus": 1,
+            "config": {"workload": "Llama-3-8B shape, 128 samples, prompts lognormal(1024, 0.8), "
+                                   "responses lognormal(378, 0.784) in [1, 2048], top-64 "
+                                   "draft-logit candidate trees, acceptance drawn from w = dl"},
+            "strategies": summary, "cost_model_cache": {"hits": hits, "misses": misses},
+            "out": out_path}
+
+
 def recorded_traffic(workload, kernel):
     """HBM bytes per launch of `kernel` on `workload` from the committed
     copy-calibrated rocprofv3 counter summary, or None when there is none or
@@ -256,6 +400,9 @@ def main():
         return
     if args.kv_migrate:
         print(json.dumps(run_kv_migrate(args)), flush=True)
+        return
+    if args.trajectory:
+        print(json.dumps(run_trajectory(args, args.trajectory)), flush=True)
         return
     if args.sweep:
         rows = run_sweep(args, args.sweep)
