@@ -37,6 +37,10 @@ def parse():
     p.add_argument("--workload", default="early",
                    help="early | tail | llama1b | sweep_b<B>_n<n> (one strategy-cost sweep cell)")
     p.add_argument("--cpu-baseline", type=int, default=1, help="0 skips the oracle timing")
+    p.add_argument("--temperature", type=float, default=0.0,
+                   help="> 0: speculative-sampling acceptance at this temperature (draft rows "
+                        "0.7 p + 0.3 random, seeded uniforms); 0: greedy")
+    p.add_argument("--eos", type=int, default=-1, help="end-of-sequence token (-1: none)")
     p.add_argument("--seed", type=int, default=None)
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="only copy BYTES device-to-device 5 times (a reference for the HBM "
@@ -419,7 +423,9 @@ def main():
     t_setup = time.time()
     W = wl.make_weights(cfg, w.seed, device="cuda")
     caps = [int(s) + len(t[0]) for s, t in zip(w.seq_lens, w.trees)]
-    ver = sv.Verifier(cfg, W, caps, max_batch=w.batch, max_tokens=w.n_tokens)
+    sampled = args.temperature > 0 or args.eos >= 0
+    ver = sv.Verifier(cfg, W, caps, max_batch=w.batch, max_tokens=w.n_tokens,
+                      sampling=args.temperature > 0)
     gen = torch.Generator(device="cuda").manual_seed(w.seed)
     for b, S in enumerate(w.seq_lens):
         k, v = ver.kv.sample_view(b)
@@ -442,13 +448,33 @@ def main():
 
     wl.follow_greedy(w.trees, w.branches, w.p_follow, greedy_fn, np.random.default_rng(w.seed))
     flat = sv.flatten_trees(w.trees)
+    q_rows = uniforms = None
+    if args.temperature > 0:
+        # draft rows: 0.7 of the target's own distribution plus 0.3 of a
+        # random one, from an untimed verify's logits; seeded uniforms
+        dbg = ver.debug_buffers(w.n_tokens, logits=True)
+        ver.verify(ids, w.trees, lens, debug=dbg)
+        q_rows = torch.empty(w.n_tokens, cfg.vocab, dtype=torch.float32, device="cuda")
+        for r0 in range(0, w.n_tokens, 256):
+            z = dbg["logits"][r0:r0 + 256].double()
+            r = torch.softmax(torch.randn(z.shape, generator=gen, device="cuda",
+                                          dtype=torch.float64) * 2.0, dim=1)
+            q = 0.7 * torch.softmax(z / args.temperature, dim=1) + 0.3 * r
+            q_rows[r0:r0 + 256] = (q / q.sum(dim=1, keepdim=True)).float()
+        del dbg
+        u = np.random.default_rng(w.seed + 1).uniform(0, 1, (w.n_tokens, 2)).astype(np.float32)
+        uniforms = torch.from_numpy(np.minimum(u, np.float32(1 - 2 ** -24))).cuda()
     torch.cuda.synchronize()
     setup_s = time.time() - t_setup
 
     stream = torch.cuda.current_stream()
 
     def step():
-        ver.verify(ids, None, lens, flat=flat, stream=stream)
+        if sampled:
+            ver.verify_sampled(ids, None, lens, args.temperature, args.eos, q_rows, uniforms,
+                               flat=flat, stream=stream)
+        else:
+            ver.verify(ids, None, lens, flat=flat, stream=stream)
         ver.commit(ids, lens, stream=stream)
 
     for _ in range(args.warmup):
@@ -541,11 +567,37 @@ def main():
         "breakdown_ms_per_step": breakdown,
         "setup_s": round(setup_s, 1),
     }
+    if sampled:
+        result["config"]["acceptance"] = (f"speculative sampling, T = {args.temperature}"
+                                          if args.temperature > 0 else "greedy") + \
+            (f", EOS token {args.eos}" if args.eos >= 0 else "")
+    if args.temperature > 0:
+        result["sampled_accept"] = sampled_accept_roofline(cfg, w, ver, breakdown["accept"],
+                                                           ms_per_step)
 
     if args.cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok,
                                               ms_per_step)
     print(json.dumps(result), flush=True)
+
+
+def sampled_accept_roofline(cfg, w, ver, accept_ms, ms_per_step):
+    """The sampled-acceptance kernel against HBM bandwidth.  Algorithmic
+    bytes: each node on a sample's walk reads its fp32 logit row, and its
+    fp32 draft row when it has children to try."""
+    acc = ver.accepted_len[:w.batch].cpu().tolist()
+    nodes = ver.accepted_nodes[:w.batch].cpu().tolist()
+    rows = 0
+    for b, (toks, pars) in enumerate(w.trees):
+        for u in nodes[b][:acc[b] + 1]:
+            rows += 2 if any(p == u for p in pars[1:]) else 1
+    alg = rows * cfg.vocab * 4
+    gbs = alg / (accept_ms / 1e3) / 1e9
+    return {"kernel": "sample_accept_kernel", "avg_launch_ms": round(accept_ms, 5),
+            "share_of_step": round(accept_ms / ms_per_step, 4), "bound": "hbm",
+            "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "work_per_launch": f"{alg} bytes ({rows} vocabulary rows of fp32)"}
 
 
 def cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok, ms_per_step):

@@ -156,6 +156,59 @@ int spec_verify(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
                 int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
                 const spec_debug* dbg);
 
+/* ---- Acceptance at a sampling temperature, and end of sequence ---------
+ *
+ * Speculative decoding is lossless (Section 2.2): at temperature T > 0 the
+ * verified tokens follow the target model's sampling distribution
+ * p_u = softmax(z_u / T) (z_u: the logits after node u).  This assumes the
+ * draft drew the children of every node u independently from its own
+ * distribution q_u.  The acceptance walk (multi-draft speculative sampling):
+ * at the current node u, with the unnormalised residual P = p_u (total R =
+ * its fp64 sum), try u's children in node order; child c with token x is
+ * accepted when uniforms[c][0] * q_u(x) * R < P(x); a rejected child sets
+ * P = max(P - R q_u, 0) and R = sum P.  An accepted child becomes u.  When no
+ * child of u is accepted (or u has none) the next token is the smallest y
+ * with P(0) + ... + P(y) > uniforms[u][1] * R.  Residuals, sums and the CDF
+ * are fp64.  accepted_len = depth of the final u, accepted_nodes = the path.
+ *
+ * End of sequence (eos_token >= 0, RLHF rollouts end at it): an accepted node
+ * carrying the EOS token ends the branch, its children are not tried and
+ * next_token = -1.  With temperature 0 the acceptance is spec_verify's greedy
+ * rule with that truncation (an accepted EOS node accepts no children).
+ *
+ * spec_sampling:
+ *   temperature  >= 0, finite
+ *   eos_token    -1 (none) or a token id
+ *   draft_probs  device [N][vocab] fp32, row i = q of node i (sums to 1;
+ *                read for nodes with children); unused when temperature == 0
+ *   uniforms     device [N][2] fp32 in [0, 1): column 0 = node i's
+ *                acceptance draw as a child, column 1 = the draw that samples
+ *                the next token if the walk ends at node i; unused at T == 0
+ * The random draws are inputs so that the caller owns the randomness. */
+typedef struct {
+  float temperature;
+  int32_t eos_token;
+  const float* draft_probs;
+  const float* uniforms;
+} spec_sampling;
+
+/* Workspace bytes spec_verify_sampled needs at temperature > 0 (the logits
+ * [N][vocab] fp32, per-row log-sum-exp and a [batch][vocab] fp64 residual on
+ * top of spec_workspace_bytes); 0 if an argument is invalid.  At temperature
+ * 0 spec_workspace_bytes suffices. */
+size_t spec_workspace_bytes_sampled(const spec_model_config* cfg, int32_t max_batch,
+                                    int32_t max_tokens);
+
+/* spec_verify with the acceptance above.  Same arguments and outputs; samp
+ * must not be NULL.  dbg->logits, when given, receives the logits the
+ * sampling reads. */
+int spec_verify_sampled(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv,
+                        int32_t batch, const int32_t* sample_ids, const int32_t* tree_offsets,
+                        const int32_t* tree_tokens, const int32_t* tree_parents,
+                        const int32_t* seq_lens, void* workspace, size_t ws_bytes, void* stream,
+                        const spec_sampling* samp, int32_t* accepted_len, int32_t* next_token,
+                        int32_t* accepted_nodes, const spec_debug* dbg);
+
 /* Commit the accepted branches of the preceding spec_verify (same batch,
  * sample_ids and seq_lens, same stream): the K/V of node accepted_nodes[b][d]
  * moves to position S_b + d for d = 1..accepted_len[b] (all layers, K and
@@ -272,7 +325,8 @@ enum {
   SPEC_K_LM_HEAD = 5,
   SPEC_K_COMMIT = 6,
   SPEC_K_TRANSFER = 7,   /* spec_kv_pack / spec_kv_unpack */
-  SPEC_K_COUNT = 8
+  SPEC_K_ACCEPT = 8,     /* tree acceptance: greedy, greedy with EOS, or sampled */
+  SPEC_K_COUNT = 9
 };
 int spec_profile_begin(int32_t kernel_class, int32_t max_launches);
 int spec_profile_end(float* total_ms, int32_t* launches);

@@ -25,6 +25,8 @@ from .binding import (  # noqa: F401
     spec_profile_end,
     spec_select_draft_count,
     spec_verify,
+    spec_verify_sampled,
     spec_workspace_bytes,
+    spec_workspace_bytes_sampled,
 )
 from .session import Verifier, flatten_trees  # noqa: F401

@@ -19,7 +19,7 @@ SPEC_MAX_TREE = 64
 STATUS = {0: "SPEC_OK", -1: "SPEC_ERR_INVALID", -2: "SPEC_ERR_TREE", -3: "SPEC_ERR_CAPACITY",
           -5: "SPEC_ERR_WORKSPACE", -6: "SPEC_ERR_UNSUPPORTED", -7: "SPEC_ERR_HIP"}
 KERNEL_CLASS = {"gemm_qkv": 0, "attention": 1, "gemm_o": 2, "gemm_gate_up": 3, "gemm_down": 4,
-                "lm_head": 5, "commit": 6}          # the kernel classes of one verify step
+                "lm_head": 5, "commit": 6, "accept": 8}   # the kernel classes of one verify step
 TRANSFER_CLASS = 7                                    # spec_kv_pack / spec_kv_unpack
 
 # Every symbol the public header declares.
@@ -27,7 +27,8 @@ EXPORTS = ("spec_kv_bytes", "spec_kv_alloc", "spec_kv_free", "spec_kv_sample_lay
            "spec_workspace_bytes", "spec_verify", "spec_kv_commit", "spec_last_error",
            "spec_profile_begin", "spec_profile_end", "spec_kv_transfer_bytes", "spec_kv_pack",
            "spec_kv_unpack", "spec_cost_model_create", "spec_cost_model_free", "spec_cost_predict",
-           "spec_cost_model_stats", "spec_select_draft_count")
+           "spec_cost_model_stats", "spec_select_draft_count", "spec_workspace_bytes_sampled",
+           "spec_verify_sampled")
 
 
 class SpecError(RuntimeError):
@@ -53,6 +54,11 @@ class spec_weights(ctypes.Structure):
 class spec_cost_coeffs(ctypes.Structure):
     _fields_ = [("c0", ctypes.c_double), ("c_seq", ctypes.c_double), ("c_draft", ctypes.c_double),
                 ("c_tree", ctypes.c_double), ("bucket_ratio", ctypes.c_double)]
+
+
+class spec_sampling(ctypes.Structure):
+    _fields_ = [("temperature", c_float), ("eos_token", c_int32), ("draft_probs", c_void_p),
+                ("uniforms", c_void_p)]
 
 
 class spec_debug(ctypes.Structure):
@@ -86,6 +92,12 @@ def lib():
                               c_void_p, c_void_p, c_void_p, c_void_p, POINTER(spec_debug)]
     L.spec_kv_commit.argtypes = [c_void_p, c_int32, i32p, i32p, c_void_p, c_void_p, c_void_p,
                                  c_void_p]
+    L.spec_workspace_bytes_sampled.argtypes = [POINTER(spec_model_config), c_int32, c_int32]
+    L.spec_workspace_bytes_sampled.restype = c_size_t
+    L.spec_verify_sampled.argtypes = [POINTER(spec_model_config), POINTER(spec_weights), c_void_p,
+                                      c_int32, i32p, i32p, i32p, i32p, i32p, c_void_p, c_size_t,
+                                      c_void_p, POINTER(spec_sampling), c_void_p, c_void_p,
+                                      c_void_p, POINTER(spec_debug)]
     L.spec_kv_transfer_bytes.argtypes = [c_void_p, c_int32, i32p, i32p]
     L.spec_kv_transfer_bytes.restype = c_size_t
     L.spec_kv_pack.argtypes = [c_void_p, c_int32, i32p, i32p, i32p, c_void_p, c_size_t, c_void_p]
@@ -104,7 +116,7 @@ def lib():
     for name in ("spec_kv_alloc", "spec_kv_free", "spec_kv_sample_layout", "spec_verify",
                  "spec_kv_commit", "spec_profile_begin", "spec_profile_end", "spec_kv_pack",
                  "spec_kv_unpack", "spec_cost_model_create", "spec_cost_model_free",
-                 "spec_cost_model_stats", "spec_select_draft_count"):
+                 "spec_cost_model_stats", "spec_select_draft_count", "spec_verify_sampled"):
         getattr(L, name).restype = c_int32
     _lib = L
     return L
@@ -242,6 +254,43 @@ def spec_verify(cfg, weights: Weights, kv: KVPool, sample_ids, tree_offsets, tre
                              _ptr(workspace), workspace.numel() * workspace.element_size(),
                              _stream(stream), _ptr(accepted_len), _ptr(next_token),
                              _ptr(accepted_nodes), ctypes.byref(dbg) if dbg else None))
+
+
+def spec_workspace_bytes_sampled(cfg, max_batch, max_tokens) -> int:
+    c = make_config(cfg)
+    return int(lib().spec_workspace_bytes_sampled(ctypes.byref(c), max_batch, max_tokens))
+
+
+def spec_verify_sampled(cfg, weights: Weights, kv: KVPool, sample_ids, tree_offsets, tree_tokens,
+                        tree_parents, seq_lens, workspace, accepted_len, next_token,
+                        accepted_nodes, temperature, eos_token=-1, draft_probs=None,
+                        uniforms=None, debug=None, stream=None):
+    """spec_verify with speculative-sampling acceptance at ``temperature`` (0:
+    greedy) and end-of-sequence truncation.  draft_probs: device fp32
+    [N][vocab]; uniforms: device fp32 [N][2]."""
+    c = make_config(cfg)
+    ids, p_ids = _i32(sample_ids)
+    offs, p_offs = _i32(tree_offsets)
+    toks, p_toks = _i32(tree_tokens)
+    pars, p_pars = _i32(tree_parents)
+    lens, p_lens = _i32(seq_lens)
+    n = int(offs[-1])
+    if temperature > 0:
+        for t, cols, what in ((draft_probs, cfg.vocab, "draft_probs"), (uniforms, 2, "uniforms")):
+            if (t is None or t.dtype != torch.float32 or not t.is_contiguous()
+                    or tuple(t.shape) != (n, cols)):
+                raise ValueError(f"{what} must be a contiguous float32 [{n}, {cols}] tensor")
+    samp = spec_sampling(float(temperature), int(eos_token), _ptr(draft_probs), _ptr(uniforms))
+    dbg = None
+    if debug:
+        dbg = spec_debug(*[debug[k].data_ptr() if debug.get(k) is not None else None
+                           for k in ("logits", "argmax", "depth", "pos", "anc")])
+    _check(lib().spec_verify_sampled(ctypes.byref(c), ctypes.byref(weights.struct), kv.handle,
+                                     len(ids), p_ids, p_offs, p_toks, p_pars, p_lens,
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     _stream(stream), ctypes.byref(samp), _ptr(accepted_len),
+                                     _ptr(next_token), _ptr(accepted_nodes),
+                                     ctypes.byref(dbg) if dbg else None))
 
 
 def spec_kv_commit(kv: KVPool, sample_ids, seq_lens, accepted_len, accepted_nodes, new_seq_lens,

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <string>
 #include <vector>
 
@@ -84,7 +85,7 @@ size_t sample_bytes(const spec_model_config* c, int32_t cap) {
 // Workspace carving; every region 256-byte aligned.
 struct WsLayout {
   size_t blob, toks, anc, rope, x, h, q, o, act, part_o, part_ml, lm_val, lm_idx, argmax, splitk,
-      total;
+      logits, resid, total;
   size_t blob_bytes;
 };
 
@@ -93,7 +94,8 @@ int64_t max_row_tiles(const spec_model_config* c, int64_t max_batch, int64_t max
   return (int64_t)c->n_kv_heads * ((max_tokens * G + 31) / 32 + max_batch);
 }
 
-WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_tokens) {
+WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_tokens,
+                   bool sampling = false) {
   WsLayout L{};
   // attention items: one per row tile and split, then padded per XCD (at most 8x)
   const int64_t items = 8 * (max_row_tiles(c, max_batch, max_tokens) + kPartCap);
@@ -122,6 +124,10 @@ WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_to
   L.lm_idx = take(max_tokens * (size_t)(c->vocab / 64) * 4);
   L.argmax = take(max_tokens * 4);
   L.splitk = take(gemm_partial_bytes());
+  if (sampling) {   // speculative sampling: fp32 logits, per-sample fp64 residual
+    L.logits = take(max_tokens * (size_t)c->vocab * 4);
+    L.resid = take(max_batch * (size_t)c->vocab * 8);
+  }
   L.total = off;
   return L;
 }
@@ -289,12 +295,13 @@ SPEC_API size_t spec_workspace_bytes(const spec_model_config* cfg, int32_t max_b
   return ws_layout(cfg, max_batch, max_tokens).total;
 }
 
-SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv,
-                         int32_t batch, const int32_t* sample_ids, const int32_t* tree_offsets,
-                         const int32_t* tree_tokens, const int32_t* tree_parents,
-                         const int32_t* seq_lens, void* workspace, size_t ws_bytes, void* stream,
-                         int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
-                         const spec_debug* dbg) {
+namespace {
+
+int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv, int32_t batch,
+                const int32_t* sample_ids, const int32_t* tree_offsets, const int32_t* tree_tokens,
+                const int32_t* tree_parents, const int32_t* seq_lens, void* workspace,
+                size_t ws_bytes, void* stream, const spec_sampling* samp, int32_t* accepted_len,
+                int32_t* next_token, int32_t* accepted_nodes, const spec_debug* dbg) {
   g_err.clear();
   // ---- validation (no side effects) ----
   if (!cfg || !w || !kv || !sample_ids || !tree_offsets || !tree_tokens || !tree_parents ||
@@ -335,14 +342,23 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
       }
     }
   }
+  const bool sampled = samp && samp->temperature > 0.f;
+  if (samp) {
+    if (!(samp->temperature >= 0.f) || !std::isfinite(samp->temperature))
+      return fail(SPEC_ERR_INVALID, "temperature must be finite and >= 0");
+    if (samp->eos_token < -1 || samp->eos_token >= cfg->vocab)
+      return fail(SPEC_ERR_INVALID, "eos_token %d out of range", samp->eos_token);
+    if (sampled && (!samp->draft_probs || !samp->uniforms))
+      return fail(SPEC_ERR_INVALID, "sampling needs draft_probs and uniforms");
+  }
   const int N = tree_offsets[batch];
-  const size_t need = ws_layout(cfg, batch, N).total;
+  const size_t need = ws_layout(cfg, batch, N, sampled).total;
   if (ws_bytes < need) return fail(SPEC_ERR_WORKSPACE, "workspace %zu bytes, needs %zu", ws_bytes, need);
 
   // ---- planning ----
   const int L = cfg->n_layers, H = cfg->hidden, nq = cfg->n_heads, nkv = cfg->n_kv_heads;
   const int hd = cfg->head_dim, G = nq / nkv, F = cfg->ffn, V = cfg->vocab;
-  const WsLayout ly = ws_layout(cfg, batch, N);
+  const WsLayout ly = ws_layout(cfg, batch, N, sampled);
   char* ws = (char*)workspace;
   hipStream_t s = (hipStream_t)stream;
 
@@ -573,14 +589,67 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
     g.n0 = g.N = V;
     g.part_val = d_lmv;
     g.part_idx = d_lmi;
-    g.logits = D.logits;
+    g.logits = D.logits ? D.logits : sampled ? (float*)(ws + ly.logits) : nullptr;
     HIP_TRY(timed(SPEC_K_LM_HEAD, s, [&] { return launch_gemm(EPI_ARGMAX, g, s); }), "lm head");
   }
   HIP_TRY(launch_argmax_reduce(d_lmv, d_lmi, N, gemm_parts(V, N, H), d_arg, D.argmax, s), "argmax");
-  HIP_TRY(launch_accept(d_si, batch, d_tok, d_par, d_toks, d_arg, accepted_len, next_token,
-                        accepted_nodes, s),
-          "accept");
+  if (sampled) {
+    const float* logits = D.logits ? D.logits : (const float*)(ws + ly.logits);
+    HIP_TRY(timed(SPEC_K_ACCEPT, s, [&] {
+              return launch_sample_accept(d_si, batch, d_tok, d_par, logits, samp->draft_probs,
+                                          samp->uniforms, V, samp->temperature, samp->eos_token,
+                                          (double*)(ws + ly.resid), accepted_len, next_token,
+                                          accepted_nodes, s);
+            }),
+            "sampled accept");
+  } else if (samp && samp->eos_token >= 0) {
+    HIP_TRY(timed(SPEC_K_ACCEPT, s, [&] {
+              return launch_accept_eos(d_si, batch, d_tok, d_par, d_toks, d_arg, samp->eos_token,
+                                       accepted_len, next_token, accepted_nodes, s);
+            }),
+            "accept");
+  } else {
+    HIP_TRY(timed(SPEC_K_ACCEPT, s, [&] {
+              return launch_accept(d_si, batch, d_tok, d_par, d_toks, d_arg, accepted_len,
+                                   next_token, accepted_nodes, s);
+            }),
+            "accept");
+  }
   return SPEC_OK;
+}
+
+}  // namespace
+
+SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv,
+                         int32_t batch, const int32_t* sample_ids, const int32_t* tree_offsets,
+                         const int32_t* tree_tokens, const int32_t* tree_parents,
+                         const int32_t* seq_lens, void* workspace, size_t ws_bytes, void* stream,
+                         int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
+                         const spec_debug* dbg) {
+  return verify_impl(cfg, w, kv, batch, sample_ids, tree_offsets, tree_tokens, tree_parents,
+                     seq_lens, workspace, ws_bytes, stream, nullptr, accepted_len, next_token,
+                     accepted_nodes, dbg);
+}
+
+SPEC_API size_t spec_workspace_bytes_sampled(const spec_model_config* cfg, int32_t max_batch,
+                                             int32_t max_tokens) {
+  std::string why;
+  if (!cfg || max_batch < 1 || max_tokens < max_batch || !config_ok(cfg, &why)) return 0;
+  return ws_layout(cfg, max_batch, max_tokens, true).total;
+}
+
+SPEC_API int spec_verify_sampled(const spec_model_config* cfg, const spec_weights* w,
+                                 spec_kv* kv, int32_t batch, const int32_t* sample_ids,
+                                 const int32_t* tree_offsets, const int32_t* tree_tokens,
+                                 const int32_t* tree_parents, const int32_t* seq_lens,
+                                 void* workspace, size_t ws_bytes, void* stream,
+                                 const spec_sampling* samp, int32_t* accepted_len,
+                                 int32_t* next_token, int32_t* accepted_nodes,
+                                 const spec_debug* dbg) {
+  if (!samp) return fail(SPEC_ERR_INVALID, "null sampling parameters");
+  return verify_impl(cfg, w, kv, batch, sample_ids, tree_offsets, tree_tokens, tree_parents,
+                     seq_lens, workspace, ws_bytes, stream, samp, accepted_len, next_token,
+                     accepted_nodes, dbg);
 }
 
 SPEC_API int spec_kv_commit(spec_kv* kv, int32_t batch, const int32_t* sample_ids,

@@ -153,6 +153,18 @@ int64_t kv_transfer_chunks(int count, int head_dim);
 hipError_t launch_kv_transfer(bool to_buffer, const MigrateInfo* info, int n, int64_t wg_per_slab,
                               int tok_total, bf16* pool, bf16* buf, int n_layers, int n_kv_heads,
                               int head_dim, hipStream_t s);
+// Speculative sampling over the trees (temperature > 0): per-row log-sum-exp
+// of logits / T, then one work-group per sample walks its tree.
+hipError_t launch_sample_accept(const SampleInfo* samples, int batch, const int32_t* tokens,
+                                const int32_t* parents, const float* logits,
+                                const float* draft_probs, const float* uniforms, int vocab,
+                                float temperature, int eos, double* resid, int32_t* accepted_len,
+                                int32_t* next_token, int32_t* accepted_nodes, hipStream_t s);
+// Greedy acceptance with an end-of-sequence token.
+hipError_t launch_accept_eos(const SampleInfo* samples, int batch, const int32_t* tokens,
+                             const int32_t* parents, const TokInfo* toks, const int32_t* argmax,
+                             int eos, int32_t* accepted_len, int32_t* next_token,
+                             int32_t* accepted_nodes, hipStream_t s);
 hipError_t launch_compact(const SampleInfo* samples, int batch, bf16* kv_pool, int n_layers,
                           int n_kv_heads, int head_dim, const int32_t* accepted_len,
                           const int32_t* accepted_nodes, int32_t* new_seq_lens, hipStream_t s);

@@ -21,11 +21,13 @@ def flatten_trees(trees):
 
 
 class Verifier:
-    def __init__(self, cfg, W, capacity, max_batch, max_tokens, device="cuda"):
+    def __init__(self, cfg, W, capacity, max_batch, max_tokens, device="cuda", sampling=False):
+        """sampling=True sizes the workspace for verify_sampled at temperature > 0."""
         self.cfg = cfg
         self.weights = B.Weights(W)
         self.kv = B.KVPool(cfg, capacity, device=device)
-        nbytes = B.spec_workspace_bytes(cfg, max_batch, max_tokens)
+        nbytes = (B.spec_workspace_bytes_sampled if sampling else B.spec_workspace_bytes)(
+            cfg, max_batch, max_tokens)
         if nbytes == 0:
             raise B.SpecError(-1, "invalid workspace request")
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
@@ -53,6 +55,17 @@ class Verifier:
         B.spec_verify(self.cfg, self.weights, self.kv, sample_ids, offsets, tokens, parents,
                       seq_lens, self.workspace, self.accepted_len, self.next_token,
                       self.accepted_nodes, debug=debug, stream=stream)
+        return self.accepted_len[:b], self.next_token[:b], self.accepted_nodes[:b]
+
+    def verify_sampled(self, sample_ids, trees, seq_lens, temperature, eos_token=-1,
+                       draft_probs=None, uniforms=None, debug=None, stream=None, flat=None):
+        """Enqueue one verify step with speculative-sampling acceptance."""
+        offsets, tokens, parents = flat if flat is not None else flatten_trees(trees)
+        b = len(sample_ids)
+        B.spec_verify_sampled(self.cfg, self.weights, self.kv, sample_ids, offsets, tokens, parents,
+                              seq_lens, self.workspace, self.accepted_len, self.next_token,
+                              self.accepted_nodes, temperature, eos_token, draft_probs, uniforms,
+                              debug=debug, stream=stream)
         return self.accepted_len[:b], self.next_token[:b], self.accepted_nodes[:b]
 
     def commit(self, sample_ids, seq_lens, stream=None):

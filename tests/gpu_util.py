@@ -20,6 +20,8 @@ Comparison rules (tolerance of the verify step on bf16 logits):
 * depth, positions, ancestor sets, compacted KV positions: bit-exact.
 """
 
+import dataclasses
+import gc
 import sys
 import time
 
@@ -206,7 +208,35 @@ def check_tree_kv(cfg, ver, ids, trees, lens, r, check_ids, layers=None):
             assert (err <= ATOL + RTOL * want.abs()).all(), f"tree {name} max err {err.max()}"
 
 
-def tiny_setup(seed=0, batch=4, chain=4, extra_cap=64):
+def device_setup(w, W_dev, cap_extra=0, seed=0, sampling=False):
+    """A Verifier for workload ``w`` with random committed K/V of the
+    workload's lengths (std of a real model's cache)."""
+    cfg = w.cfg
+    caps = [int(s) + len(t[0]) + cap_extra for s, t in zip(w.seq_lens, w.trees)]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=w.batch, max_tokens=w.n_tokens,
+                      sampling=sampling)
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    for b, S in enumerate(w.seq_lens):
+        k, v = ver.kv.sample_view(b)
+        wl.fill_prefix_kv(k, v, int(S), wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    return ver
+
+
+def release(*objs):
+    for o in objs:
+        del o
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def shallow(w, layers=2):
+    """The same workload on a ``layers``-deep model of the same shape."""
+    w.cfg = dataclasses.replace(w.cfg, n_layers=layers)
+    return w
+
+
+def tiny_setup(seed=0, batch=4, chain=4, extra_cap=64, sampling=False):
     """The 2-layer workload: bf16-rounded weights, oracle prefill of each
     128-token prompt written into the pool, root = the oracle's greedy token
     after the prompt, chain drafts following the oracle's greedy choice."""
@@ -217,7 +247,7 @@ def tiny_setup(seed=0, batch=4, chain=4, extra_cap=64):
              "lm_head": W_cpu["lm_head"].cuda(),
              "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
     caps = [int(s) + extra_cap for s in w.seq_lens]
-    ver = sv.Verifier(cfg, W_dev, caps, max_batch=batch, max_tokens=batch * 64)
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=batch, max_tokens=batch * 64, sampling=sampling)
     for b, prompt in enumerate(w.prompts):
         pk, pv, logits = oracle.prefill(cfg, W_cpu, prompt, cache_dtype=torch.bfloat16)
         k, v = ver.kv.sample_view(b)

@@ -225,3 +225,68 @@ def test_transfer_bytes_and_validation(fake):
         assert L.spec_last_error()
     # nothing to move: accepted without device work
     assert L.spec_kv_pack(fake.kv, 1, i32(0), i32(4), i32(4), buf, 0, None) == 0
+
+
+def test_sampled_workspace_adds_logits_and_residual():
+    cfg = wl.LLAMA_8B
+    for b, n in [(1, 1), (4, 256), (128, 1024)]:
+        plain = sv.spec_workspace_bytes(cfg, b, n)
+        samp = sv.spec_workspace_bytes_sampled(cfg, b, n)
+        extra = n * cfg.vocab * 4 + b * cfg.vocab * 8
+        assert extra <= samp - plain < extra + 512
+    assert sv.spec_workspace_bytes_sampled(cfg, 0, 8) == 0
+
+
+def sampled_call(f, samp, ws_bytes=None, trees=None):
+    ids, lens = [0, 1], [10, 10]
+    trees = trees or [GOOD, GOOD]
+    offs, toks, pars = sv.flatten_trees(trees)
+    if ws_bytes is None:
+        ws_bytes = sv.spec_workspace_bytes_sampled(f.cfg, len(ids), int(offs[-1]))
+    (a1, p1), (a2, p2), (a3, p3), (a4, p4), (a5, p5) = (B._i32(ids), B._i32(offs), B._i32(toks),
+                                                        B._i32(pars), B._i32(lens))
+    rc = f.L.spec_verify_sampled(ctypes.byref(f.c), ctypes.byref(f.w), f.kv, len(ids), p1, p2, p3,
+                                 p4, p5, ctypes.c_void_p(FAKE_DEV), ws_bytes, None,
+                                 ctypes.byref(samp) if samp is not None else None,
+                                 ctypes.c_void_p(FAKE_DEV), ctypes.c_void_p(FAKE_DEV),
+                                 ctypes.c_void_p(FAKE_DEV), None)
+    return rc, f.L.spec_last_error().decode()
+
+
+@pytest.mark.parametrize("case", ["null", "neg_t", "nan_t", "inf_t", "eos_high", "eos_low",
+                                  "no_q", "no_u", "plain_ws", "tree"])
+def test_sampled_validation(fake, case):
+    """Malformed sampled calls fail before any device work (fake device
+    pointers are never dereferenced)."""
+    samp = B.spec_sampling(0.8, -1, FAKE_DEV, FAKE_DEV)
+    ws, trees, code = None, None, -1
+    if case == "null":
+        samp = None
+    elif case == "neg_t":
+        samp.temperature = -0.5
+    elif case == "nan_t":
+        samp.temperature = float("nan")
+    elif case == "inf_t":
+        samp.temperature = float("inf")
+    elif case == "eos_high":
+        samp.eos_token = fake.cfg.vocab
+    elif case == "eos_low":
+        samp.eos_token = -2
+    elif case == "no_q":
+        samp.draft_probs = None
+    elif case == "no_u":
+        samp.uniforms = None
+    elif case == "plain_ws":
+        ws, code = sv.spec_workspace_bytes(fake.cfg, 2, 6), -5
+    elif case == "tree":
+        trees, code = [GOOD, ([1, 2], [-1, 1])], -2
+    rc, msg = sampled_call(fake, samp, ws, trees)
+    assert rc == code, msg
+    assert msg
+
+
+def test_sampled_workspace_beyond_4gib():
+    """Sizes are size_t end to end (a 16384-node sampled call needs over
+    4 GiB for its fp32 logits alone)."""
+    n = sv.spec_workspace_bytes_sampled(wl.LLAMA_8B, 512, 16384)
+    assert n > 16384 * wl.LLAMA_8B.vocab * 4 > 1 << 32

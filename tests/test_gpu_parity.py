@@ -6,8 +6,6 @@ benchmark times) and are compared on seeded subsets of samples, which is
 exact because samples never interact in a verify step.
 """
 
-import dataclasses
-import gc
 
 import numpy as np
 import pytest
@@ -17,8 +15,9 @@ import oracle
 import paper_2512_04752_amd as sv
 import workload as wl
 from tests.gpu_util import (ATOL, check_argmax, check_logits, check_sample_acceptance,
-                            check_tree_kv, cpu_weights, full_check, oracle_greedy_fn,
-                            prefix_for_oracle, run_gpu, say, split_rows, tiny_setup)
+                            check_tree_kv, cpu_weights, device_setup, full_check,
+                            oracle_greedy_fn, prefix_for_oracle, release, run_gpu, say, shallow,
+                            split_rows, tiny_setup)
 
 pytestmark = pytest.mark.gpu
 
@@ -181,31 +180,6 @@ def test_tiny_multistep_matches_greedy_decoding():
 # ---------------------------------------------------------------------------
 # full-size workloads: the real 1B / 8B kernel shapes
 # ---------------------------------------------------------------------------
-
-def device_setup(w, W_dev, cap_extra=0, seed=0):
-    cfg = w.cfg
-    caps = [int(s) + len(t[0]) + cap_extra for s, t in zip(w.seq_lens, w.trees)]
-    ver = sv.Verifier(cfg, W_dev, caps, max_batch=w.batch, max_tokens=w.n_tokens)
-    gen = torch.Generator(device="cuda").manual_seed(seed)
-    for b, S in enumerate(w.seq_lens):
-        k, v = ver.kv.sample_view(b)
-        wl.fill_prefix_kv(k, v, int(S), wl.prefix_kv_std(cfg), gen)
-    torch.cuda.synchronize()
-    return ver
-
-
-def release(*objs):
-    for o in objs:
-        del o
-    gc.collect()
-    torch.cuda.empty_cache()
-
-
-def shallow(w, layers=2):
-    """The same workload on a ``layers``-deep model of the same shape."""
-    w.cfg = dataclasses.replace(w.cfg, n_layers=layers)
-    return w
-
 
 @pytest.mark.parametrize("name", ["llama1b", "early", "tail"])
 def test_two_layer_full_shape(name):
