@@ -593,7 +593,8 @@ def sampled_accept_roofline(cfg, w, ver, accept_ms, ms_per_step):
             rows += 2 if any(p == u for p in pars[1:]) else 1
     alg = rows * cfg.vocab * 4
     gbs = alg / (accept_ms / 1e3) / 1e9
-    return {"kernel": "sample_accept_kernel", "avg_launch_ms": round(accept_ms, 5),
+    return {"kernel": "node_decide_kernel<1024> + sample_walk_kernel<1024>",
+            "avg_launch_ms": round(accept_ms, 5),
             "share_of_step": round(accept_ms / ms_per_step, 4), "bound": "hbm",
             "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(gbs / PEAK_HBM_GBS, 4),

@@ -124,9 +124,9 @@ WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_to
   L.lm_idx = take(max_tokens * (size_t)(c->vocab / 64) * 4);
   L.argmax = take(max_tokens * 4);
   L.splitk = take(gemm_partial_bytes());
-  if (sampling) {   // speculative sampling: fp32 logits, per-sample fp64 residual
+  if (sampling) {   // speculative sampling: fp32 logits, node decisions, fp64 residual rows
     L.logits = take(max_tokens * (size_t)c->vocab * 4);
-    L.resid = take(max_batch * (size_t)c->vocab * 8);
+    L.resid = take(sample_accept_scratch((int)max_batch, (int)max_tokens, c->vocab));
   }
   L.total = off;
   return L;
@@ -596,9 +596,9 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
   if (sampled) {
     const float* logits = D.logits ? D.logits : (const float*)(ws + ly.logits);
     HIP_TRY(timed(SPEC_K_ACCEPT, s, [&] {
-              return launch_sample_accept(d_si, batch, d_tok, d_par, logits, samp->draft_probs,
-                                          samp->uniforms, V, samp->temperature, samp->eos_token,
-                                          (double*)(ws + ly.resid), accepted_len, next_token,
+              return launch_sample_accept(d_si, batch, N, d_toks, d_tok, d_par, logits,
+                                          samp->draft_probs, samp->uniforms, V, samp->temperature,
+                                          samp->eos_token, ws + ly.resid, accepted_len, next_token,
                                           accepted_nodes, s);
             }),
             "sampled accept");

@@ -155,10 +155,14 @@ hipError_t launch_kv_transfer(bool to_buffer, const MigrateInfo* info, int n, in
                               int head_dim, hipStream_t s);
 // Speculative sampling over the trees (temperature > 0): per-row log-sum-exp
 // of logits / T, then one work-group per sample walks its tree.
-hipError_t launch_sample_accept(const SampleInfo* samples, int batch, const int32_t* tokens,
+// Scratch of launch_sample_accept: per-node decisions and one fp64 vocabulary
+// row per sample.
+size_t sample_accept_scratch(int batch, int n_tokens, int vocab);
+hipError_t launch_sample_accept(const SampleInfo* samples, int batch, int n_tokens,
+                                const TokInfo* toks, const int32_t* tokens,
                                 const int32_t* parents, const float* logits,
                                 const float* draft_probs, const float* uniforms, int vocab,
-                                float temperature, int eos, double* resid, int32_t* accepted_len,
+                                float temperature, int eos, void* scratch, int32_t* accepted_len,
                                 int32_t* next_token, int32_t* accepted_nodes, hipStream_t s);
 // Greedy acceptance with an end-of-sequence token.
 hipError_t launch_accept_eos(const SampleInfo* samples, int batch, const int32_t* tokens,

@@ -11,7 +11,7 @@ sampled from (the debug dump), with the same draft rows and uniforms.
 Accepted path and next token must be identical wherever every decision's
 margin (relative distance of the acceptance test from its threshold,
 distance of the uniform from the chosen CDF interval's edges) exceeds
-1e-9; below that the two fp64 computations may round to different sides,
+1e-11; below that the two fp64 computations may round to different sides,
 and only validity is checked.  Greedy acceptance with EOS takes integer
 inputs and is bit-exact.
 """
@@ -28,7 +28,7 @@ from tests.gpu_util import (cpu_weights, device_setup, release, run_gpu, say, sh
 
 pytestmark = pytest.mark.gpu
 
-MARGIN = 1e-9
+MARGIN = 1e-11
 U_MAX = np.float32(1.0 - 2.0 ** -24)
 
 
@@ -39,10 +39,12 @@ def depths_of(parents):
     return d
 
 
-def fill_tokens_by_level(ver, ids, trees, lens, T, mix, seed):
+def fill_tokens_by_level(ver, ids, trees, lens, T, mix, seed, anti=False):
     """Draw every non-root token from its parent's q = mix p + (1 - mix) r
     (p the target at temperature T from the GPU's logits, r a random
-    softmax); returns the draft rows q [N, V] (fp32, on the device)."""
+    softmax, or with ``anti`` softmax(-3 z / T), a draft that favours the
+    target's least likely tokens); returns the draft rows q [N, V] (fp32,
+    on the device)."""
     V = ver.cfg.vocab
     offs = split_rows(trees)
     N = offs[-1]
@@ -58,8 +60,11 @@ def fill_tokens_by_level(ver, ids, trees, lens, T, mix, seed):
         ridx = torch.tensor(rows, device="cuda")
         z = out_dbg["logits"][ridx].double()
         p = torch.softmax(z / T, dim=1)
-        r = torch.softmax(torch.randn(len(rows), V, generator=gen, device="cuda",
-                                      dtype=torch.float64) * 2.0, dim=1)
+        if anti:
+            r = torch.softmax(-3.0 * z / T, dim=1)
+        else:
+            r = torch.softmax(torch.randn(len(rows), V, generator=gen, device="cuda",
+                                          dtype=torch.float64) * 2.0, dim=1)
         q = mix * p + (1.0 - mix) * r
         q = (q / q.sum(dim=1, keepdim=True)).float()
         q_all[ridx] = q
@@ -152,6 +157,49 @@ def test_tiny_sampled_matches_oracle(T):
     say(f"  exact {exact}, excused {excused}, samples with accepts {accepted}, "
         f"with a rejection {rejected}")
     assert exact >= 15 and accepted > 0 and rejected > 0
+    release(ver, W_dev)
+
+
+def rejections(pars, path):
+    """Children rejected at each node of an accepted path (the oracle's walk):
+    those before the taken child, all of them at the last node."""
+    out = []
+    for k, u in enumerate(path):
+        kids = SA.children(pars, u)
+        out.append(kids.index(path[k + 1]) if k + 1 < len(path) else len(kids))
+    return out
+
+
+def test_tiny_sampled_wide_star():
+    """Roots with 20 to 40 children drawn from a draft that favours the
+    target's least likely tokens: nodes with more than eight rejected
+    children continue on the stored residual row."""
+    cfg, w, W_cpu, W_dev, ver = tiny_setup(seed=7, batch=8, extra_cap=64, sampling=True)
+    rng = np.random.default_rng(95)
+    trees = []
+    for b in range(w.batch):
+        n = int(rng.integers(21, 42))
+        par = [-1] + [0] * (n - 1)
+        if b % 2:                                   # a second level under the first child
+            par = par[:n - 6] + [1] * 6
+        trees.append(([w.trees[b][0][0]] + [0] * (n - 1), par))
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    q_all = fill_tokens_by_level(ver, ids, trees, lens, 1.0, mix=0.02, seed=96, anti=True)
+    N = sum(len(t[0]) for t in trees)
+    U = uniforms_for(N, 97)
+    dbg = ver.debug_buffers(N, logits=True)
+    acc, nxt, nodes = ver.verify_sampled(ids, trees, lens, 1.0, -1, q_all,
+                                         torch.from_numpy(U).cuda(), debug=dbg)
+    torch.cuda.synchronize()
+    out = {"logits": dbg["logits"].cpu(), "accepted_len": acc.cpu().tolist(),
+           "next_token": nxt.cpu().tolist(), "nodes": nodes.cpu()}
+    exact, excused, accepted, rejected = check_sampled(trees, out, q_all, U, 1.0, -1)
+    most = 0
+    for b, (toks, pars) in enumerate(trees):
+        L = out["accepted_len"][b]
+        most = max(most, max(rejections(pars, out["nodes"][b][:L + 1].tolist())))
+    say(f"  exact {exact}, excused {excused}, most rejections at one node {most}")
+    assert exact >= 7 and most > 8
     release(ver, W_dev)
 
 
