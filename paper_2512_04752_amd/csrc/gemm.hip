@@ -11,7 +11,7 @@
 //   EPI_ARGMAX   LM head: per row, the (max, lowest index) over each wave's
 //                column slab, optionally also the fp32 logits
 //
-// Structure (one 256-thread work-group = 4 waves in a WM x WN grid, output
+// Structure (one work-group = NW = 4 or 8 waves in a WM x WN grid, output
 // tile BM x BN, each wave BM/WM x BN/WN built from 32 x 32
 // v_mfma_f32_32x32x16_bf16 blocks; K step BK = 64 or 32):
 //   * operand tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 (no
@@ -28,10 +28,12 @@
 //     consecutive rows, one chunk) hit all 64 LDS banks once;
 //   * fragments of the next 16-wide k-step are read from LDS into a second
 //     register set while the current set feeds the MFMAs.
-// Tile shapes (pick_tile): 256 x 256 (4 waves of 128 x 128, 4 stages of 32)
-// and 256 x 128 (128 x 64 per wave, 3 stages) for many rows, 128 x 128 (2 or
-// 4 stages) for up to 128 rows or narrow products, and 32 x 256 / 64 x 256
-// (3 stages) for few rows, where the weights are streamed.  Work-groups are
+// Tile shapes (pick_tile): 256 x 256 (8 waves of 128 x 64, 4 stages of 32)
+// and 256 x 128 (8 waves of 64 x 64, 3 stages of 64) for many rows: two
+// waves per SIMD, so one wave's MFMAs cover the other's waits and barrier;
+// 128 x 128 (4 waves, 4 stages) for up to 128 rows or narrow products, and
+// 32 x 256 / 64 x 256 (4 waves, 3 stages) for few rows, where the weights
+// are streamed.  Work-groups are
 // dealt round-robin over the 8 XCDs; the tile order is remapped so that the
 // M tiles sharing one weight tile run on one XCD and hit its L2.
 //
@@ -46,7 +48,6 @@ namespace spec {
 
 namespace {
 
-constexpr int NT = 256;
 constexpr size_t kPartialCap = 64ull << 20;   // bytes of split-K partials (workspace)
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -155,17 +156,18 @@ constexpr int gemm_occupancy() {
   return (NS * (BM + BN) * BK * 2 <= 80 * 1024 && BM * BN <= 256 * 128) ? 2 : 1;
 }
 
-template <int EPI, int BM, int BN, int WM, int NS, int BK>
-__global__ __launch_bounds__(NT, (gemm_occupancy<BM, BN, NS, BK>())) void gemm_bf16_kernel(GemmArgs a) {
-  constexpr int WN = 4 / WM;
+template <int EPI, int BM, int BN, int WM, int NS, int BK, int NW = 4>
+__global__ __launch_bounds__(NW * 64, (gemm_occupancy<BM, BN, NS, BK>())) void gemm_bf16_kernel(GemmArgs a) {
+  constexpr int WN = NW / WM;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
   constexpr int ROWB = BK * 2, CPR = BK / 8, RPL = 1024 / ROWB;  // row bytes, chunks, rows per load
   constexpr int KS = BK / 16;                                     // MFMA k-steps per K step
   constexpr int A_BYTES = BM * ROWB, STAGE = (BM + BN) * ROWB;
-  constexpr int A_LOADS = A_BYTES / 1024 / 4, B_LOADS = BN * ROWB / 1024 / 4;
+  constexpr int A_LOADS = A_BYTES / 1024 / NW, B_LOADS = BN * ROWB / 1024 / NW;
   constexpr int LPW = A_LOADS + B_LOADS;    // wave-loads per wave and stage
   static_assert(BK == 32 || BK == 64, "K step");
-  static_assert(MB >= 1 && NB >= 2 && A_LOADS >= 1, "tile shape");
+  static_assert(MB >= 1 && NB >= 2 && A_LOADS >= 1 && B_LOADS >= 1, "tile shape");
+  static_assert(A_BYTES % (1024 * NW) == 0 && BN * ROWB % (1024 * NW) == 0, "loads per wave");
   static_assert(NS >= 2 && (NS - 2) * LPW <= 63, "ring depth (vmcnt holds at most 63)");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
@@ -399,21 +401,19 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   }
 }
 
-enum TileShape { TILE_256x256, TILE_256x128, TILE_128x128_2WG, TILE_128x128, TILE_64x256, TILE_32x256 };
+enum TileShape { TILE_256x256, TILE_256x128, TILE_128x128, TILE_64x256, TILE_32x256 };
 
 // Shape choice (measured over the verify step's products at 32 to 1024 rows):
 //   * few rows: 32- or 64-row tiles that stream 256 weight rows each;
 //   * up to 128 rows: 128 x 128 tiles with a 4-stage ring (one work-group per
 //     CU, deep lookahead for the weight stream);
 //   * many rows and at least 384 256 x 256 tiles (gate/up, LM head): 256 x 256
-//     tiles, which need the fewest operand bytes per flop, with 32-wide K
-//     steps in a 4-stage ring (128 KB; 3-5 % faster than 64-wide steps in
-//     two stages);
-//   * the q/k/v projection at 512 rows and more: 128 x 128 tiles with a
-//     2-stage ring, two work-groups per CU, so that one group's epilogue
-//     (rotary, scattered cache writes) overlaps the other's main loop;
-//   * otherwise 256 x 128 tiles with a 3-stage ring, or, for products too
-//     narrow to give 64 of them, 128 x 128 tiles with split K.
+//     tiles, which need the fewest operand bytes per flop, 8 waves, with
+//     32-wide K steps in a 4-stage ring (128 KB; 3-5 % faster than 64-wide
+//     steps in two stages);
+//   * otherwise (the q/k/v projection from 512 rows on included) 256 x 128
+//     tiles, 8 waves, 64-wide K steps in a 3-stage ring (144 KB), or, for
+//     products too narrow to give 64 of them, 128 x 128 tiles with split K.
 // 256-wide tiles need every weight segment (q/k/v) to be a multiple of 256 so
 // no tile straddles two; 128-wide ones need multiples of 128.
 TileShape pick_tile(int epi, int M, int N, int K, int n0, int n1) {
@@ -422,7 +422,6 @@ TileShape pick_tile(int epi, int M, int N, int K, int n0, int n1) {
   if (w256 && M <= 64) return TILE_64x256;
   if (M <= 128) return TILE_128x128;
   if (w256 && M > 128 && (long)((M + 255) / 256) * (N / 256) >= 384) return TILE_256x256;
-  if (epi == EPI_QKV && M >= 512) return TILE_128x128_2WG;
   if ((long)((M + 255) / 256) * (N / 128) < 64 && K <= 4096) return TILE_128x128;
   return TILE_256x128;
 }
@@ -439,19 +438,19 @@ int choose_splits(int epi, int BM, int BK, long tiles, int M, int N, int K) {
   return s;
 }
 
-template <int EPI, int BM, int BN, int WM, int NS, int BK = 64>
+template <int EPI, int BM, int BN, int WM, int NS, int BK = 64, int NW = 4>
 hipError_t launch_tile(GemmArgs a, hipStream_t s) {
   constexpr int SMEM = NS * (BM + BN) * BK * 2;
   static bool configured = false;
   if (!configured) {
-    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN, WM, NS, BK>,
+    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<EPI, BM, BN, WM, NS, BK, NW>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
     if (e != hipSuccess) return e;
     configured = true;
   }
   const long tiles = (long)((a.M + BM - 1) / BM) * (a.N / BN);
   a.ksplit = a.partial ? choose_splits(EPI, BM, BK, tiles, a.M, a.N, a.K) : 1;
-  gemm_bf16_kernel<EPI, BM, BN, WM, NS, BK><<<(unsigned)(tiles * a.ksplit), NT, SMEM, s>>>(a);
+  gemm_bf16_kernel<EPI, BM, BN, WM, NS, BK, NW><<<(unsigned)(tiles * a.ksplit), NW * 64, SMEM, s>>>(a);
   if (a.ksplit > 1) {
     const size_t threads = (size_t)a.M * (a.N / 2);
     splitk_reduce_kernel<EPI, BN><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
@@ -462,9 +461,8 @@ hipError_t launch_tile(GemmArgs a, hipStream_t s) {
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
   switch (pick_tile(EPI, a.M, a.N, a.K, a.n0, a.n1)) {
-    case TILE_256x256: return launch_tile<EPI, 256, 256, 2, 4, 32>(a, s);
-    case TILE_256x128: return launch_tile<EPI, 256, 128, 2, 3>(a, s);
-    case TILE_128x128_2WG: return launch_tile<EPI, 128, 128, 2, 2>(a, s);
+    case TILE_256x256: return launch_tile<EPI, 256, 256, 2, 4, 32, 8>(a, s);
+    case TILE_256x128: return launch_tile<EPI, 256, 128, 4, 3, 64, 8>(a, s);
     case TILE_32x256: return launch_tile<EPI, 32, 256, 1, 3>(a, s);
     case TILE_64x256: return launch_tile<EPI, 64, 256, 2, 3>(a, s);
     default: return launch_tile<EPI, 128, 128, 2, 4>(a, s);
@@ -475,7 +473,6 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
 
 int gemm_parts(int N, int M, int K) {
   switch (pick_tile(EPI_ARGMAX, M, N, K, N, 0)) {
-    case TILE_256x256: return N / 128;
     case TILE_64x256: return N / 128;
     default: return N / 64;       // 256x128, 128x128 and 32x256: wave slabs of 64 columns
   }
