@@ -28,9 +28,14 @@
 //
 //   * tree_attention_kernel: one 32-row tile per work-group (at most 32 query
 //     rows per KV head, e.g. 8-node trees with 4 query heads per KV head).  The
-//     key range is dealt to the 4 waves in 32-key blocks; each wave streams
-//     its blocks through a private LDS ring (no work-group barrier), and the
-//     four partial softmax states are merged through LDS at the end.
+//     key range is dealt to the work-group's 2 waves in 32-key blocks; each
+//     wave streams its blocks through a private 40 KB LDS ring of
+//     half-stages (the K or the V rows of one block; the K of block t is
+//     waited for before the V, and three half-stages stay in flight), with no
+//     work-group barrier, and the partial softmax states are merged through
+//     LDS at the end.  Two such work-groups share a CU, so one's start-up
+//     (descriptor, query and first-block latency) and merge overlap the
+//     other's streaming.
 //   * tree_attention_wide_kernel<HD, NW>: 32*NW query rows per work-group
 //     (NW = 4 or 8 waves; larger trees).  Wave w owns rows 32w..32w+31; all
 //     waves share a ring of 64-key K/V stages loaded cooperatively, so the
@@ -48,13 +53,20 @@ namespace spec {
 
 namespace {
 
-constexpr int NT = 256, KBLK = 32;
+constexpr int KBLK = 32;
 
-typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
+// Direct global -> LDS load: 16 bytes per lane, landing at the wave-uniform
+// LDS address `lds` + 16 * lane.  Issued as inline assembly so that the
+// compiler does not track an LDS write in flight: it cannot tell which ring
+// stage a load targets, and would make every transposing V read wait for all
+// outstanding loads (vmcnt(0)), which collapses the ring's lookahead.  The
+// rings' own vmcnt waits and barriers order these loads.
 __device__ __forceinline__ void load_lds16(const void* g, void* lds) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
+  const uint32_t m0 = (uint32_t)(uintptr_t)(lds_char*)lds;
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0) : "memory", "m0");
 }
 
 // Physical 16-byte chunk of logical chunk c in K row `key`: 16 consecutive
@@ -278,16 +290,17 @@ __device__ __forceinline__ void store_row(const AttnArgs& a, const f32x16 (&o)[H
 template <int HD>
 struct AttnCfg {
   static constexpr int ROW = HD * 2;                    // bytes per K or V row
-  // narrow kernel: per-wave ring of 32-key blocks
-  static constexpr int NST = HD == 128 ? 2 : 4;
+  // narrow kernel: per-wave ring of half-stages (the K or the V rows of one
+  // 32-key block), 40 KB per wave, so four waves fill the CU's 160 KB
   static constexpr int KV_BYTES = KBLK * ROW;
-  static constexpr int STAGE = 2 * KV_BYTES;
-  static constexpr int WAVE_RING = NST * STAGE;         // 32 KB per wave
+  static constexpr int WAVE_RING = 40 * 1024;
+  static constexpr int NH = WAVE_RING / KV_BYTES;       // half-stage slots: 5 (HD 128), 10 (HD 64)
   static constexpr int LOADS = KV_BYTES / 1024;         // wave-loads for K (and for V)
   static constexpr int ROWS_PER_LOAD = 1024 / ROW;
   static constexpr int O_STRIDE = HD + 1;               // floats per merge row
-  static constexpr int MERGE_BYTES = 4 * 32 * O_STRIDE * 4 + 4 * 32 * 2 * 4;
-  static constexpr int SMEM = (4 * WAVE_RING) > MERGE_BYTES ? (4 * WAVE_RING) : MERGE_BYTES;
+  static constexpr int NWN = 2;                         // waves per work-group
+  static constexpr int MERGE_BYTES = NWN * 32 * O_STRIDE * 4 + NWN * 32 * 2 * 4;
+  static constexpr int SMEM = (NWN * WAVE_RING) > MERGE_BYTES ? (NWN * WAVE_RING) : MERGE_BYTES;
   // wide kernels: shared ring of 64-key stages
   static constexpr int WKEYS = 64;
   static constexpr int W_KV = WKEYS * ROW;              // K (or V) bytes per stage
@@ -301,12 +314,23 @@ constexpr int wide_stages() {
   return (NW == 8 || HD == 64) ? 4 : 2;
 }
 
+// Wait until at most n (< N) of this wave's half-stage loads, L
+// vector-memory operations each, are outstanding (n is wave-uniform).
+template <int L, int N>
+__device__ __forceinline__ void wait_halves(int n) {
+  if constexpr (N <= 1) {
+    wait_vm<0>();
+  } else {
+    if (n >= N - 1) wait_vm<(N - 1) * L>();
+    else wait_halves<L, N - 1>(n);
+  }
+}
+
 template <int HD>
-__global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
+__global__ __launch_bounds__(AttnCfg<HD>::NWN * 64, 2) void tree_attention_kernel(AttnArgs a) {
   using C = AttnCfg<HD>;
   constexpr int DC = HD / 8;                  // 16-byte chunks per row
   constexpr int NB = HD / 32;                 // 32-dim output blocks
-  constexpr int LPS = 2 * C::LOADS;           // wave-loads per stage
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   // Items are dealt round-robin over the 8 XCDs; remap so that consecutive
@@ -342,23 +366,26 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
 
   // Blocks of this wave: w, w+4, w+8, ... of the item's range.
   const int nblk = (it.key1 - it.key0 + KBLK - 1) / KBLK;
-  const int mine = nblk > w ? (nblk - w + 3) / 4 : 0;
+  const int mine = nblk > w ? (nblk - w + C::NWN - 1) / C::NWN : 0;
   const int mask_from = min(si.seq_len, it.key1);   // blocks ending past this need the mask
 
-  // Lane l of wave-load j copies row (j*ROWS_PER_LOAD + l / DC) of the block
-  // into physical chunk l % DC; keys past the range repeat the last key,
-  // whose scores are masked.
+  // Half-stage h of this wave is the K rows (h even) or the V rows (h odd)
+  // of its block h/2, in ring slot h % NH.  Lane l of wave-load j copies row
+  // (j*ROWS_PER_LOAD + l / DC) into physical chunk l % DC; keys past the
+  // range repeat the last key, whose scores are masked.
   const int lrow = lane / DC, lch = lane % DC;
-  auto issue = [&](int t, int slot) {
-    const int kb = it.key0 + (w + 4 * t) * KBLK;
-    char* st = ring + slot * C::STAGE;
+  auto issue = [&](int hs) {
+    const int kb = it.key0 + (w + C::NWN * (hs >> 1)) * KBLK;
+    char* st = ring + (hs % C::NH) * C::KV_BYTES;
+    const bool is_v = hs & 1;
+    const bf16* src = is_v ? vbase : kbase;
 #pragma unroll
     for (int j = 0; j < C::LOADS; ++j) {
       const int row = j * C::ROWS_PER_LOAD + lrow;
       int key = kb + row;
       key = key < it.key1 ? key : it.key1 - 1;
-      load_lds16(kbase + (size_t)key * HD + ((lch ^ kswz<HD>(row)) << 3), st + j * 1024);
-      load_lds16(vbase + (size_t)key * HD + ((lch ^ vswz(row)) << 3), st + C::KV_BYTES + j * 1024);
+      const int sw = is_v ? vswz(row) : kswz<HD>(row);
+      load_lds16(src + (size_t)key * HD + ((lch ^ sw) << 3), st + j * 1024);
     }
   };
 
@@ -368,21 +395,24 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < NB; ++i) o[i] = f32x16{};
 
+  // NH - 2 half-stages ahead of the block being read: while block t is
+  // multiplied, the K and V of block t+1 and the K of block t+2 (at HD 128)
+  // are in flight.
+  const int nh = 2 * mine;
 #pragma unroll
-  for (int t = 0; t < C::NST - 1; ++t)
-    if (t < mine) issue(t, t);
+  for (int hs = 0; hs < C::NH - 2; ++hs)
+    if (hs < nh) issue(hs);
 
   for (int t = 0; t < mine; ++t) {
-    // Keep NST-1 blocks in flight: issue block t+NST-1 into the slot of block
-    // t-1 (consumed in the previous iteration), then wait for block t.
-    if (t + C::NST - 1 < mine) {
-      issue(t + C::NST - 1, (t + C::NST - 1) % C::NST);
-      wait_vm<LPS * (C::NST - 1)>();
-    } else {
-      wait_vm<0>();
-    }
-    const char* st = ring + (t % C::NST) * C::STAGE;
-    const int kb = it.key0 + (w + 4 * t) * KBLK;
+    // The slots of block t-1 (consumed in the previous iteration) take
+    // half-stages 2t+NH-2 and 2t+NH-1.
+    if (2 * t + C::NH - 2 < nh) issue(2 * t + C::NH - 2);
+    if (2 * t + C::NH - 1 < nh) issue(2 * t + C::NH - 1);
+    const int newest = min(2 * t + C::NH - 1, nh - 1);
+    wait_halves<C::LOADS, C::NH>(newest - 2 * t);          // K of block t has landed
+    const char* st = ring + ((2 * t) % C::NH) * C::KV_BYTES;
+    const char* sv = ring + ((2 * t + 1) % C::NH) * C::KV_BYTES;
+    const int kb = it.key0 + (w + C::NWN * t) * KBLK;
 
     // S^T = K . Q^T for the 32 keys of this block (two independent chains).
     f32x16 s0 = f32x16{}, s1 = f32x16{};
@@ -396,14 +426,15 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
     bf16x8 pb[2];
     softmax_any<NB>(kb + KBLK > mask_from, s, kb, it.key1, si.seq_len, anc_row, h, sl2, m_run, l_run,
                     o, pb);
-    pv_block<HD>(st + C::KV_BYTES, pb, o, lane);
+    wait_halves<C::LOADS, C::NH>(newest - 2 * t - 1);      // V of block t has landed
+    pv_block<HD>(sv, pb, o, lane);
   }
   l_run += __shfl_xor(l_run, 32);
 
-  // Merge the four waves' (m, l, O) through LDS.
+  // Merge the waves' (m, l, O) through LDS.
   __syncthreads();
   float* o_sh = (float*)smem;
-  float* ml_sh = o_sh + 4 * 32 * C::O_STRIDE;
+  float* ml_sh = o_sh + C::NWN * 32 * C::O_STRIDE;
   if (h == 0) {
     ml_sh[(w * 32 + r) * 2] = m_run;
     ml_sh[(w * 32 + r) * 2 + 1] = l_run;
@@ -417,17 +448,17 @@ __global__ __launch_bounds__(NT, 1) void tree_attention_kernel(AttnArgs a) {
     }
   __syncthreads();
 
-  for (int idx = tid; idx < 32 * HD; idx += NT) {
+  for (int idx = tid; idx < 32 * HD; idx += C::NWN * 64) {
     const int row = idx / HD, d = idx % HD;
     const int gr = it.row0 + row;
     const int nd = gr / G, hq = it.kvh * G + gr % G;
     if (nd >= si.ntok) continue;
     float M = -INFINITY;
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) M = fmaxf(M, ml_sh[(ww * 32 + row) * 2]);
+    for (int ww = 0; ww < C::NWN; ++ww) M = fmaxf(M, ml_sh[(ww * 32 + row) * 2]);
     float O = 0.f, L = 0.f;
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) {
+    for (int ww = 0; ww < C::NWN; ++ww) {
       const float mw = ml_sh[(ww * 32 + row) * 2];
       const float f = (mw == -INFINITY) ? 0.f : fast_exp2(mw - M);
       O += f * o_sh[(ww * 32 + row) * C::O_STRIDE + d];
@@ -638,7 +669,7 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
     configured = true;
   }
   hipError_t e = hipSuccess;
-  if (a.n_items) tree_attention_kernel<HD><<<(a.n_items + 7) / 8 * 8, NT, C::SMEM, s>>>(a);
+  if (a.n_items) tree_attention_kernel<HD><<<(a.n_items + 7) / 8 * 8, C::NWN * 64, C::SMEM, s>>>(a);
   if (a.n_wide && e == hipSuccess) e = launch_wide<HD, 4>(a, a.wide, a.n_wide, s);
   if (a.n_wide8 && e == hipSuccess) e = launch_wide<HD, 8>(a, a.wide8, a.n_wide8, s);
   if (e != hipSuccess) return e;
