@@ -369,8 +369,8 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
                        tree_offsets[b + 1] - tree_offsets[b], 0, 0};
   }
   // Split-KV plan.  A row tile is 32 query rows of one (sample, kv head).  A
-  // (sample, kv head) with one tile gets narrow items (4 waves dealing the
-  // keys among themselves, one work-group per CU); 2-4 tiles get one 4-wave
+  // (sample, kv head) with one tile gets narrow items (2 waves dealing the
+  // keys among themselves, two work-groups per CU); 2-4 tiles get one 4-wave
   // wide group (two per CU); more get 8-wave groups of 8 tiles (one per CU).
   // Every (sample, kv head) key range is cut into chunks of `chunk` keys,
   // sized so that the whole call is about kTargetSlots chunk-sized CU
@@ -378,7 +378,10 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
   // per range and at most kPartCap partial states.
   auto tiles_of = [&](int b) { return (si[b].ntok * G + 31) / 32; };
   auto keys_of = [&](int b) { return (int64_t)si[b].seq_len + si[b].ntok; };
-  auto cu_weight = [&](int tiles) {       // CU occupancy of one chunk's work-groups
+  // Cost weight of one chunk's work-groups: their CU occupancy, except that a
+  // narrow item counts as a whole CU (measured: sizing its chunks as half a
+  // CU's worth, i.e. twice as many splits, is slower).
+  auto cu_weight = [&](int tiles) {
     return tiles == 1 ? 1.0 : tiles <= 4 ? 0.5 : (double)((tiles + 7) / 8);
   };
   int64_t max_keys = 0;
