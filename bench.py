@@ -63,8 +63,8 @@ def run_sweep(args, out_path):
     {1,4,16,64,256} x draft-tree budget n in {1,4,8,16,32,64} (top-n nodes by
     draft logit), one pool of 256 samples with lognormal KV lengths (median
     2048, sigma 0.8, clipped to [128, 16384]); a batch-B cell uses the first B
-    samples.  Per cell: verify+commit latency, verified and accepted tokens/s
-    and the composite roofline fraction."""
+    samples.  Per cell: verify+commit latency (median over the timed steps),
+    verified and accepted tokens/s and the composite roofline fraction."""
     import torch
 
     import paper_2512_04752_amd as sv
@@ -108,12 +108,17 @@ def run_sweep(args, out_path):
                     ver.verify(ids, None, lens, flat=flat, stream=stream)
                     ver.commit(ids, lens, stream=stream)
                 torch.cuda.synchronize()
-                t0 = time.perf_counter()
-                for _ in range(args.steps):
+                # Median of the per-step times (HIP events on the launch stream),
+                # so that one slow step does not move a cell of the cost surface.
+                evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                       for _ in range(args.steps)]
+                for e0, e1 in evs:
+                    e0.record(stream)
                     ver.verify(ids, None, lens, flat=flat, stream=stream)
                     ver.commit(ids, lens, stream=stream)
+                    e1.record(stream)
                 torch.cuda.synchronize()
-                ms = (time.perf_counter() - t0) * 1e3 / args.steps
+                ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in evs]))
                 acc = int(ver.accepted_len[:B].sum().item()) + B
                 N = w.n_tokens
                 kv = sum(S + len(t[0]) for S, t in zip(lens, w.trees))
