@@ -542,8 +542,21 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
   aa.comb = d_comb;
   aa.n_comb = (int)comb.size();
 
+  // Every RMSNorm after the first follows a residual product (O or down
+  // projection); when that product is split over K the norm runs inside its
+  // split-K reduction, otherwise on its own.
+  auto resid_then_norm = [&](int kind, GemmArgs g, const void* gain, const char* what) -> int {
+    bool fused = false;
+    g.norm_gain = (const bf16*)gain;
+    g.norm_out = d_h;
+    g.norm_eps = cfg->rms_eps;
+    g.norm_done = &fused;
+    HIP_TRY(timed(kind, s, [&] { return launch_gemm(EPI_RESID, g, s); }), what);
+    if (!fused) HIP_TRY(launch_rmsnorm(d_x, (const bf16*)gain, d_h, N, H, cfg->rms_eps, s), "rmsnorm");
+    return SPEC_OK;
+  };
+  HIP_TRY(launch_rmsnorm(d_x, (const bf16*)w->attn_norm[0], d_h, N, H, cfg->rms_eps, s), "rmsnorm");
   for (int l = 0; l < L; ++l) {
-    HIP_TRY(launch_rmsnorm(d_x, (const bf16*)w->attn_norm[l], d_h, N, H, cfg->rms_eps, s), "rmsnorm");
     GemmArgs g = ga;
     g.A = d_h;
     g.K = H;
@@ -564,8 +577,7 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
     g.B0 = (const bf16*)w->wo[l];
     g.n0 = g.N = H;
     g.x = d_x;
-    HIP_TRY(timed(SPEC_K_GEMM_O, s, [&] { return launch_gemm(EPI_RESID, g, s); }), "o gemm");
-    HIP_TRY(launch_rmsnorm(d_x, (const bf16*)w->ffn_norm[l], d_h, N, H, cfg->rms_eps, s), "rmsnorm");
+    if (int rc = resid_then_norm(SPEC_K_GEMM_O, g, w->ffn_norm[l], "o gemm")) return rc;
     g = ga;
     g.A = d_h;
     g.K = H;
@@ -581,9 +593,9 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
     g.B0 = (const bf16*)w->w_down[l];
     g.n0 = g.N = H;
     g.x = d_x;
-    HIP_TRY(timed(SPEC_K_GEMM_DOWN, s, [&] { return launch_gemm(EPI_RESID, g, s); }), "down gemm");
+    const void* next_norm = l + 1 < L ? w->attn_norm[l + 1] : w->final_norm;
+    if (int rc = resid_then_norm(SPEC_K_GEMM_DOWN, g, next_norm, "down gemm")) return rc;
   }
-  HIP_TRY(launch_rmsnorm(d_x, (const bf16*)w->final_norm, d_h, N, H, cfg->rms_eps, s), "rmsnorm");
   {
     GemmArgs g = ga;
     g.A = d_h;

@@ -99,6 +99,14 @@ struct GemmArgs {
   // the split count the launcher picked.
   float* partial;
   int ksplit;
+  // EPI_RESID: the RMSNorm that follows the product (norm_out = bf16 of
+  // x / rms(x) * norm_gain, row-major [M][N]); NULL: none.  When the product
+  // is split over K, the launcher fuses the norm into the split-K reduction
+  // and sets *norm_done; otherwise the caller runs the norm itself.
+  const bf16* norm_gain;
+  bf16* norm_out;
+  float norm_eps;
+  bool* norm_done;
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);

@@ -401,6 +401,88 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   }
 }
 
+// Split-K reduction of a residual product fused with the RMSNorm that
+// follows it: x += (sum of the splits, in split order), then
+// norm_out = bf16(x / sqrt(mean(x^2) + eps) * gain), one 256-thread block per
+// row, CPT 4-float chunks of the row per thread (N <= 1024 * CPT).  Bitwise
+// the same as splitk_reduce_kernel followed by the stand-alone RMSNorm (same
+// summation orders), one pass over the row fewer.  Every chunk's split loads
+// are issued together, since few rows mean few blocks to hide latency with.
+template <int CPT>
+__global__ __launch_bounds__(256) void splitk_reduce_norm_kernel(GemmArgs a) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  float* xr = a.x + (size_t)row * a.N;
+  const size_t plane = (size_t)a.M * a.N;
+  const float* pr = a.partial + (size_t)row * a.N;
+  f32x4 v[CPT], t[CPT];
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) t[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int s = 0;
+  for (; s + 4 <= a.ksplit; s += 4) {
+    f32x4 p[4][CPT];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int k = 0; k < CPT; ++k) {
+        const int c = (threadIdx.x + 256 * k) * 4;
+        p[q][k] = c < a.N ? *(const f32x4*)(pr + (s + q) * plane + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int k = 0; k < CPT; ++k) t[k] += p[q][k];
+  }
+  for (; s < a.ksplit; ++s)
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int c = (threadIdx.x + 256 * k) * 4;
+      if (c < a.N) t[k] += *(const f32x4*)(pr + s * plane + c);
+    }
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < a.N) {
+      v[k] = *(const f32x4*)(xr + c) + t[k];
+      *(f32x4*)(xr + c) = v[k];
+      ss += v[k][0] * v[k][0] + v[k][1] * v[k][1] + v[k][2] * v[k][2] + v[k][3] * v[k][3];
+    }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float rstd = rsqrtf(tot / (float)a.N + a.norm_eps);
+  bf16* orow = a.norm_out + (size_t)row * a.N;
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < a.N) {
+      const bf16x4 g = *(const bf16x4*)(a.norm_gain + c);
+      bf16x4 y;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) y[j] = (bf16)(v[k][j] * rstd * (float)g[j]);
+      *(bf16x4*)(orow + c) = y;
+    }
+  }
+}
+
+// Launch the fused reduction + norm; false when the row is too long for it.
+bool launch_reduce_norm(const GemmArgs& a, hipStream_t s) {
+  const int cpt = (a.N + 1023) / 1024;
+  switch (cpt) {
+    case 1: splitk_reduce_norm_kernel<1><<<(unsigned)a.M, 256, 0, s>>>(a); return true;
+    case 2: splitk_reduce_norm_kernel<2><<<(unsigned)a.M, 256, 0, s>>>(a); return true;
+    case 3:
+    case 4: splitk_reduce_norm_kernel<4><<<(unsigned)a.M, 256, 0, s>>>(a); return true;
+    case 5: case 6: case 7:
+    case 8: splitk_reduce_norm_kernel<8><<<(unsigned)a.M, 256, 0, s>>>(a); return true;
+    default: return false;
+  }
+}
+
 enum TileShape { TILE_256x256, TILE_256x128, TILE_128x128, TILE_64x256, TILE_32x256 };
 
 // Shape choice (measured over the verify step's products at 32 to 1024 rows):
@@ -452,8 +534,12 @@ hipError_t launch_tile(GemmArgs a, hipStream_t s) {
   a.ksplit = a.partial ? choose_splits(EPI, BM, BK, tiles, a.M, a.N, a.K) : 1;
   gemm_bf16_kernel<EPI, BM, BN, WM, NS, BK, NW><<<(unsigned)(tiles * a.ksplit), NW * 64, SMEM, s>>>(a);
   if (a.ksplit > 1) {
-    const size_t threads = (size_t)a.M * (a.N / 2);
-    splitk_reduce_kernel<EPI, BN><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
+    if (EPI == EPI_RESID && a.norm_out != nullptr && a.N % 4 == 0 && launch_reduce_norm(a, s)) {
+      if (a.norm_done) *a.norm_done = true;
+    } else {
+      const size_t threads = (size_t)a.M * (a.N / 2);
+      splitk_reduce_kernel<EPI, BN><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(a);
+    }
   }
   return hipGetLastError();
 }
