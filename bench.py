@@ -579,11 +579,28 @@ def main():
     if args.temperature > 0:
         result["sampled_accept"] = sampled_accept_roofline(cfg, w, ver, breakdown["accept"],
                                                            ms_per_step)
+    result["compaction"] = compaction_roofline(cfg, w, ver, breakdown["commit"])
 
     if args.cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok,
                                               ms_per_step)
     print(json.dumps(result), flush=True)
+
+
+def compaction_roofline(cfg, w, ver, commit_ms):
+    """The KV compaction of one commit against HBM bandwidth.  Algorithmic
+    bytes: every accepted node not already at its final slot (node index !=
+    depth) has its K and V rows of every layer and KV head read once and
+    written once."""
+    acc = ver.accepted_len[:w.batch].cpu().tolist()
+    nodes = ver.accepted_nodes[:w.batch].cpu().tolist()
+    moved = sum(1 for b in range(w.batch) for dd in range(1, acc[b] + 1) if nodes[b][dd] != dd)
+    row_bytes = cfg.n_layers * 2 * cfg.n_kv_heads * cfg.head_dim * 2
+    alg = 2 * moved * row_bytes
+    gbs = alg / (commit_ms / 1e3) / 1e9 if commit_ms > 0 else 0.0
+    return {"bound": "hbm", "moved_rows": moved, "bytes_per_commit": alg,
+            "ms_per_commit": commit_ms, "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "kernel": "compact_kernel"}
 
 
 def sampled_accept_roofline(cfg, w, ver, accept_ms, ms_per_step):

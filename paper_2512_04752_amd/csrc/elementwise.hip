@@ -150,46 +150,55 @@ __global__ void accept_kernel(const SampleInfo* samples, int batch, const int32_
   }
 }
 
-// Move the accepted branch of one (sample, layer, K/V head) to positions
-// S_b + 1 .. S_b + accepted_len.  Sources (S_b + node, node >= depth) can be
-// destinations of shallower entries, so every source row is read into
-// registers before any row is written.
+// Move the accepted branch of one sample, for one layer and a group of K/V heads, to positions
+// S_b + 1 .. S_b + accepted_len: row d takes the row of node path[d] > d (rows with path[d] == d
+// stay).  Every row written before row d lies below d, and every source of row d or later lies
+// above it, so the chunks go in passes of increasing d.  Within a pass a source can be the
+// destination of a deeper row, so each pass reads all its chunks into registers, the work-group
+// synchronises, and then the pass writes.
 template <int HD>
 __global__ __launch_bounds__(256) void compact_kernel(const SampleInfo* samples, bf16* kv_pool,
-                                                      int n_kv_heads, const int32_t* accepted_len,
+                                                      int n_kv_heads, int heads_per_wg,
+                                                      const int32_t* accepted_len,
                                                       const int32_t* accepted_nodes,
                                                       int32_t* new_seq_lens) {
-  constexpr int DC = HD / 8;
-  constexpr int PER = (kMaxTree * DC + 255) / 256;
-  const int b = blockIdx.x, layer = blockIdx.y, kvh2 = blockIdx.z;
+  constexpr int DC = HD / 8;  // 16-byte chunks per row of one head
+  constexpr int PER = 8;      // chunks per thread and pass
+  const int b = blockIdx.x, layer = blockIdx.y;
   const SampleInfo s = samples[b];
   int acc = accepted_len[b];
   if (acc < 0) acc = 0;
   if (acc > s.ntok - 1) acc = s.ntok - 1;
   if (s.seq_len + acc >= s.cap) acc = s.cap - 1 - s.seq_len;
-  if (layer == 0 && kvh2 == 0 && threadIdx.x == 0) new_seq_lens[b] = s.seq_len + acc + 1;
+  if (layer == 0 && blockIdx.z == 0 && threadIdx.x == 0) new_seq_lens[b] = s.seq_len + acc + 1;
   if (acc == 0) return;
-  bf16* base = kv_pool + s.kv_base + ((size_t)layer * 2 * n_kv_heads + kvh2) * s.cap * HD;
+  const size_t head_stride = (size_t)s.cap * HD;
+  bf16* base = kv_pool + s.kv_base +
+               ((size_t)layer * 2 * n_kv_heads + (size_t)blockIdx.z * heads_per_wg) * head_stride;
   const int32_t* nodes = accepted_nodes + (size_t)b * kMaxTree;
-  i32x4 v[PER];
-  int dst[PER];
+  const int per_row = heads_per_wg * DC, total = acc * per_row;
+  for (int q0 = 0; q0 < total; q0 += 256 * PER) {
+    i32x4 v[PER];
+    int64_t dst[PER];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int q = threadIdx.x + 256 * k;
-    const int d = 1 + q / DC, c = q % DC;
-    dst[k] = -1;
-    if (d <= acc) {
-      const int nd = nodes[d];
-      if (nd > d && nd < s.ntok && s.seq_len + nd < s.cap) {
-        v[k] = *(const i32x4*)(base + (size_t)(s.seq_len + nd) * HD + c * 8);
-        dst[k] = (s.seq_len + d) * HD + c * 8;
+    for (int k = 0; k < PER; ++k) {
+      const int q = q0 + threadIdx.x + 256 * k;
+      dst[k] = -1;
+      if (q < total) {
+        const int d = 1 + q / per_row, r = q % per_row;
+        const int nd = nodes[d];
+        if (nd > d && nd < s.ntok && s.seq_len + nd < s.cap) {
+          const int64_t col = (int64_t)(r / DC) * head_stride + (r % DC) * 8;
+          v[k] = *(const i32x4*)(base + col + (int64_t)(s.seq_len + nd) * HD);
+          dst[k] = col + (int64_t)(s.seq_len + d) * HD;
+        }
       }
     }
-  }
-  __syncthreads();
+    __syncthreads();
 #pragma unroll
-  for (int k = 0; k < PER; ++k)
-    if (dst[k] >= 0) *(i32x4*)(base + dst[k]) = v[k];
+    for (int k = 0; k < PER; ++k)
+      if (dst[k] >= 0) *(i32x4*)(base + dst[k]) = v[k];
+  }
 }
 
 }  // namespace
@@ -240,12 +249,21 @@ hipError_t launch_accept(const SampleInfo* samples, int batch, const int32_t* to
 hipError_t launch_compact(const SampleInfo* samples, int batch, bf16* kv_pool, int n_layers,
                           int n_kv_heads, int head_dim, const int32_t* accepted_len,
                           const int32_t* accepted_nodes, int32_t* new_seq_lens, hipStream_t s) {
-  const dim3 grid(batch, n_layers, 2 * n_kv_heads);
+  // Head groups split each (sample, layer) only as far as it takes to give the launch about
+  // a thousand work-groups: at large batch one work-group moves all K/V heads of a layer.
+  const int heads = 2 * n_kv_heads;
+  int groups = 1;
+  while (groups < heads && (int64_t)batch * n_layers * groups < 1024) {
+    ++groups;
+    while (heads % groups) ++groups;
+  }
+  const dim3 grid(batch, n_layers, groups);
+  const int hpw = heads / groups;
   if (head_dim == 128)
-    compact_kernel<128><<<grid, 256, 0, s>>>(samples, kv_pool, n_kv_heads, accepted_len,
+    compact_kernel<128><<<grid, 256, 0, s>>>(samples, kv_pool, n_kv_heads, hpw, accepted_len,
                                              accepted_nodes, new_seq_lens);
   else if (head_dim == 64)
-    compact_kernel<64><<<grid, 256, 0, s>>>(samples, kv_pool, n_kv_heads, accepted_len,
+    compact_kernel<64><<<grid, 256, 0, s>>>(samples, kv_pool, n_kv_heads, hpw, accepted_len,
                                             accepted_nodes, new_seq_lens);
   else
     return hipErrorInvalidValue;
