@@ -533,10 +533,7 @@ def main():
                 "kernel": "gemm_bf16_kernel<EPI_GATE_UP> (+ split-K reduce)",
                 "work_per_launch": f"{gu_bytes} bytes (gate and up weights once, rows in and out)"}
     else:
-        kv_bytes = sum((int(S) + len(t[0])) for S, t in zip(w.seq_lens, w.trees)) * \
-            cfg.n_kv_heads * d * 2 * 2
-        qo_bytes = n_tok * cfg.n_heads * d * 2 * 2
-        work = kv_bytes + qo_bytes
+        work = attention_work(cfg, w)
         achieved = work / (avg_ms / 1e3) / 1e9
         kern = " + ".join(attention_kernels(cfg, w) + [f"attention_combine_kernel<{d}>"])
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
@@ -579,12 +576,35 @@ def main():
     if args.temperature > 0:
         result["sampled_accept"] = sampled_accept_roofline(cfg, w, ver, breakdown["accept"],
                                                            ms_per_step)
+    result["attention"] = attention_roofline(cfg, w, breakdown["attention"])
     result["compaction"] = compaction_roofline(cfg, w, ver, breakdown["commit"])
 
     if args.cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, W, ver, w, plain_trees, lens, n_tok,
                                               ms_per_step)
     print(json.dumps(result), flush=True)
+
+
+def attention_work(cfg, w):
+    """Algorithmic bytes of one layer's tree attention: the K and V rows of
+    every committed and tree key once, the queries in and the outputs out."""
+    d = cfg.head_dim
+    kv_bytes = sum((int(S) + len(t[0])) for S, t in zip(w.seq_lens, w.trees)) * \
+        cfg.n_kv_heads * d * 2 * 2
+    qo_bytes = w.n_tokens * cfg.n_heads * d * 2 * 2
+    return kv_bytes + qo_bytes
+
+
+def attention_roofline(cfg, w, attn_ms):
+    """Tree attention of one step (every layer, split-KV merge included)
+    against HBM bandwidth, whichever kernel class dominates the step."""
+    alg = attention_work(cfg, w) * cfg.n_layers
+    gbs = alg / (attn_ms / 1e3) / 1e9 if attn_ms > 0 else 0.0
+    return {"bound": "hbm", "bytes_per_step": alg, "ms_per_step": attn_ms,
+            "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "kernel": " + ".join(attention_kernels(cfg, w) +
+                                 [f"attention_combine_kernel<{cfg.head_dim}>"])}
 
 
 def compaction_roofline(cfg, w, ver, commit_ms):

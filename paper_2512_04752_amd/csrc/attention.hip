@@ -602,45 +602,65 @@ __global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void tree_attention_wide_
   store_row<HD>(a, o, m_run, l_run, it.nsplit, it.part + w * it.nsplit, r, h, si.tok0 + node, head);
 }
 
-// Merge the partial states of a row tile's key ranges: one block per query
-// row, one thread per head dimension; the per-split weights are computed once
-// into LDS and every split's partial output is an independent load.
+// Merge the partial states of a row tile's key ranges.  A 256-thread block
+// takes RPB query rows of one item with HD/4 lanes per row, four consecutive
+// dimensions per lane.  A row's lanes share its splits' (m, l) to form the
+// split weights, and every split's partial output is one 16-byte load per
+// lane, four splits in flight at a time, accumulated in split order.
 template <int HD>
-__global__ __launch_bounds__(HD) void attention_combine_kernel(AttnArgs a) {
-  constexpr int MAXS = 64;
-  __shared__ float wgt[MAXS];
-  __shared__ float inv_l;
+__global__ __launch_bounds__(256) void attention_combine_kernel(AttnArgs a) {
+  constexpr int LPR = HD / 4, RPB = 256 / LPR, MAXS = 64;
+  __shared__ float wgt[RPB][MAXS];
+  __shared__ float inv_l[RPB];
   const CombineItem ci = a.comb[blockIdx.x];
-  const int row = blockIdx.y;
+  const int lane = threadIdx.x % LPR, rr = threadIdx.x / LPR;
+  const int row = blockIdx.y * RPB + rr;
   const SampleInfo si = a.samples[ci.sample];
   const int G = a.n_heads / a.n_kv_heads;
   const int gr = ci.row0 + row;
   const int nd = gr / G, hq = ci.kvh * G + gr % G;
-  if (nd >= si.ntok) return;
-  const int d = threadIdx.x;
-  if (d < 64) {
-    float M = -INFINITY;
-    for (int sp = d; sp < ci.nsplit; sp += 64)
-      M = fmaxf(M, a.part_ml[((size_t)(ci.part0 + sp) * 32 + row) * 2]);
+  const bool live = nd < si.ntok;
+  const int ns = live ? ci.nsplit : 0;
+  float M = -INFINITY;
+  for (int sp = lane; sp < ns; sp += LPR)
+    M = fmaxf(M, a.part_ml[((size_t)(ci.part0 + sp) * 32 + row) * 2]);
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) M = fmaxf(M, __shfl_xor(M, m));
-    float L = 0.f;
-    for (int sp = d; sp < ci.nsplit; sp += 64) {
-      const size_t slot = (size_t)(ci.part0 + sp) * 32 + row;
-      const float ms = a.part_ml[slot * 2];
-      const float f = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M);
-      if (sp < MAXS) wgt[sp] = f;
-      L += f * a.part_ml[slot * 2 + 1];
-    }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) L += __shfl_xor(L, m);
-    if (d == 0) inv_l = 1.f / L;
+  for (int m = LPR / 2; m >= 1; m >>= 1) M = fmaxf(M, __shfl_xor(M, m));
+  float L = 0.f;
+  for (int sp = lane; sp < ns; sp += LPR) {
+    const size_t slot = (size_t)(ci.part0 + sp) * 32 + row;
+    const float ms = a.part_ml[slot * 2];
+    const float f = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M);
+    wgt[rr][sp] = f;
+    L += f * a.part_ml[slot * 2 + 1];
   }
+#pragma unroll
+  for (int m = LPR / 2; m >= 1; m >>= 1) L += __shfl_xor(L, m);
+  if (lane == 0) inv_l[rr] = 1.f / L;
   __syncthreads();
-  float O = 0.f;
-  for (int sp = 0; sp < ci.nsplit; ++sp)
-    O += wgt[sp] * a.part_o[((size_t)(ci.part0 + sp) * 32 + row) * HD + d];
-  a.out[(size_t)(si.tok0 + nd) * a.n_heads * HD + hq * HD + d] = (bf16)(O * inv_l);
+  if (!live) return;
+  const float* src = a.part_o + ((size_t)ci.part0 * 32 + row) * HD + 4 * lane;
+  constexpr size_t STRIDE = (size_t)32 * HD;   // floats between consecutive splits
+  f32x4 O = {0.f, 0.f, 0.f, 0.f};
+  int sp = 0;
+  for (; sp + 4 <= ns; sp += 4) {
+    f32x4 p[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) p[u] = *(const f32x4*)(src + (sp + u) * STRIDE);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) O[j] += wgt[rr][sp + u] * p[u][j];
+  }
+  for (; sp < ns; ++sp) {
+    const f32x4 p = *(const f32x4*)(src + sp * STRIDE);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) O[j] += wgt[rr][sp] * p[j];
+  }
+  bf16x4 v;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = (bf16)(O[j] * inv_l[rr]);
+  *(bf16x4*)(a.out + (size_t)(si.tok0 + nd) * a.n_heads * HD + hq * HD + 4 * lane) = v;
 }
 
 template <int HD, int NW>
@@ -673,7 +693,8 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   if (a.n_wide && e == hipSuccess) e = launch_wide<HD, 4>(a, a.wide, a.n_wide, s);
   if (a.n_wide8 && e == hipSuccess) e = launch_wide<HD, 8>(a, a.wide8, a.n_wide8, s);
   if (e != hipSuccess) return e;
-  if (a.n_comb) attention_combine_kernel<HD><<<dim3(a.n_comb, 32), HD, 0, s>>>(a);
+  if (a.n_comb)
+    attention_combine_kernel<HD><<<dim3(a.n_comb, 32 / (256 / (HD / 4))), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 
