@@ -327,7 +327,7 @@ __global__ __launch_bounds__(NW * 64, (gemm_occupancy<BM, BN, NS, BK>())) void g
           if (row < a.M) xcol[(size_t)row * a.N + j * 32] = xv[e] + acc[i][j][e];
         }
       }
-  } else if constexpr (EPI == EPI_GATE_UP || EPI == EPI_QKV) {
+  } else if constexpr (EPI == EPI_GATE_UP) {
 #pragma unroll
     for (int p = 0; p < NB / 2; ++p)
 #pragma unroll
@@ -336,12 +336,72 @@ __global__ __launch_bounds__(NW * 64, (gemm_occupancy<BM, BN, NS, BK>())) void g
         for (int e = 0; e < 16; ++e) {
           const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
           if (row >= a.M) continue;
-          const int P = wn * (NB / 2) + p;
-          if constexpr (EPI == EPI_QKV)
-            epi_qkv<BN>(a, row, tn, P, c, acc[i][2 * p][e], acc[i][2 * p + 1][e]);
-          else
-            epi_gate_up<BN>(a, row, tn, P, c, acc[i][2 * p][e], acc[i][2 * p + 1][e]);
+          epi_gate_up<BN>(a, row, tn, wn * (NB / 2) + p, c, acc[i][2 * p][e], acc[i][2 * p + 1][e]);
         }
+  } else if constexpr (EPI == EPI_QKV) {
+    // The same arithmetic as epi_qkv, with the segment and head taken once
+    // per wave and, for each 32-row block, every row's rotary angles and
+    // destination fetched before any is used, so those loads (and the
+    // token -> sample -> cache slot chain of K and V rows) are in flight
+    // together instead of one row after another.
+    const int vs = tn * BN;
+    const int seg = vs < a.n0 ? 0 : (vs < a.n0 + a.n1 ? 1 : 2);
+    const int local = vs - (seg == 0 ? 0 : (seg == 1 ? a.n0 : a.n0 + a.n1));
+    const int hd = a.head_dim, qpd = hd / 64, half = hd / 2;
+#pragma unroll
+    for (int p = 0; p < NB / 2; ++p) {
+      const int P = wn * (NB / 2) + p;
+      const int head = local / hd + P / qpd;
+      const int fi = (P % qpd) * 32 + c;
+#pragma unroll
+      for (int i = 0; i < MB; ++i) {
+        float2 cs[16];
+        bf16* dst[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+          row = row < a.M ? row : a.M - 1;        // loads only; stores are guarded below
+          cs[e] = seg < 2 ? a.rope_cs[(size_t)row * half + fi] : float2{1.f, 0.f};
+        }
+        if (seg == 0) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+            dst[e] = a.q_out + (size_t)row * a.n0 + head * hd + fi;
+          }
+        } else {
+          int smp[16], node[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+            row = row < a.M ? row : a.M - 1;
+            smp[e] = a.toks[row].sample;
+            node[e] = a.toks[row].node;
+          }
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const SampleInfo sv = a.samples[smp[e]];
+            dst[e] = a.kv_pool + sv.kv_base +
+                     ((((size_t)a.layer * 2 + (seg - 1)) * a.n_kv_heads + head) * sv.cap + sv.seq_len +
+                      node[e]) * hd + fi;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+          if (row >= a.M) continue;
+          float x1 = acc[i][2 * p][e], x2 = acc[i][2 * p + 1][e];
+          if (seg < 2) {
+            const float y1 = x1 * cs[e].x - x2 * cs[e].y;
+            const float y2 = x2 * cs[e].x + x1 * cs[e].y;
+            x1 = y1;
+            x2 = y2;
+          }
+          dst[e][0] = (bf16)x1;
+          dst[e][half] = (bf16)x2;
+        }
+      }
+    }
   } else {  // EPI_ARGMAX: one partial (max, lowest index) per row and wave slab of TN columns
     const int col0 = tn * BN + wn * TN + c;
     const int parts = a.N / TN;
