@@ -9,29 +9,34 @@ namespace spec {
 
 namespace {
 
-// Depth, position and ancestor set of every node: one thread per sample
-// walks its tree in node order (parents come first).
-__global__ void tree_meta_kernel(const SampleInfo* samples, int batch, const int32_t* parents,
-                                 TokInfo* toks, uint64_t* anc, int32_t* dbg_depth,
-                                 int32_t* dbg_pos, uint64_t* dbg_anc) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+// Depth, position and ancestor set of every node: one wave per sample, lane
+// i = node i (a tree has at most 64 nodes).  Pointer jumping: lane i holds
+// the set of its ancestors at distance < 2^r and its ancestor at distance
+// 2^r (the root points at itself); six rounds of "set |= set of that
+// ancestor, jump to its jump" cover every depth up to 63.  Depth is the set's
+// size minus one.
+__global__ __launch_bounds__(256) void tree_meta_kernel(const SampleInfo* samples, int batch,
+                                                        const int32_t* parents, TokInfo* toks,
+                                                        uint64_t* anc, int32_t* dbg_depth,
+                                                        int32_t* dbg_pos, uint64_t* dbg_anc) {
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6), i = threadIdx.x & 63;
   if (b >= batch) return;
   const SampleInfo s = samples[b];
-  for (int i = 0; i < s.ntok; ++i) {
-    const int row = s.tok0 + i;
-    int depth = 0;
-    uint64_t set = 1ull;
-    if (i > 0) {
-      const int p = parents[row];
-      depth = toks[s.tok0 + p].depth + 1;
-      set = anc[s.tok0 + p] | (1ull << i);
-    }
-    toks[row] = TokInfo{b, i, s.seq_len + depth, depth};
-    anc[row] = set;
-    if (dbg_depth) dbg_depth[row] = depth;
-    if (dbg_pos) dbg_pos[row] = s.seq_len + depth;
-    if (dbg_anc) dbg_anc[row] = set;
+  const bool live = i < s.ntok;
+  int jump = (live && i > 0) ? parents[s.tok0 + i] : i;
+  uint64_t set = 1ull << i;
+#pragma unroll
+  for (int r = 0; r < 6; ++r) {
+    set |= __shfl(set, jump);
+    jump = __shfl(jump, jump);
   }
+  if (!live) return;
+  const int row = s.tok0 + i, depth = __popcll(set) - 1;
+  toks[row] = TokInfo{b, i, s.seq_len + depth, depth};
+  anc[row] = set;
+  if (dbg_depth) dbg_depth[row] = depth;
+  if (dbg_pos) dbg_pos[row] = s.seq_len + depth;
+  if (dbg_anc) dbg_anc[row] = set;
 }
 
 // cos/sin of position * theta^(-2j/d), angles in double precision.
@@ -206,8 +211,8 @@ __global__ __launch_bounds__(256) void compact_kernel(const SampleInfo* samples,
 hipError_t launch_tree_meta(const SampleInfo* samples, int batch, const int32_t* parents,
                             TokInfo* toks, uint64_t* anc, int32_t* dbg_depth, int32_t* dbg_pos,
                             uint64_t* dbg_anc, hipStream_t s) {
-  tree_meta_kernel<<<(batch + 63) / 64, 64, 0, s>>>(samples, batch, parents, toks, anc, dbg_depth,
-                                                     dbg_pos, dbg_anc);
+  tree_meta_kernel<<<(batch + 3) / 4, 256, 0, s>>>(samples, batch, parents, toks, anc, dbg_depth,
+                                                    dbg_pos, dbg_anc);
   return hipGetLastError();
 }
 
