@@ -45,7 +45,11 @@ numerators, the attention output, the SwiGLU activation; weights and cached
 K/V already are bfloat16) and keeps everything else exact.  That is an ideal
 bf16-operand computation of the same definition; the tests use it only to
 measure how far bf16 storage alone moves the logits of a deep random-weight
-model, which sets the tolerance for full-depth comparisons.
+model, which sets the tolerance for full-depth comparisons.  It is pinned
+against an independent decoder with the same storage points rounded (the
+Hugging Face Llama in float64 with rounding hooks, each branch decoded on its
+own), and each of its rounding points is shown to matter by a planted
+omission.
 """
 
 from __future__ import annotations
@@ -322,14 +326,15 @@ def commit(prefix_k, prefix_v, seq_lens, result, cache_dtype=torch.bfloat16):
     return out_k, out_v, out_s
 
 
-def prefill(cfg, W, prompt, cache_dtype=torch.bfloat16):
+def prefill(cfg, W, prompt, cache_dtype=torch.bfloat16, operand_dtype=None):
     """K/V of a prompt: the prompt is a chain whose every token sees all
     earlier ones (causal), starting at position 0.  Returns (K, V, logits)
     with K, V of shape [L, nkv, len(prompt), d] rounded to ``cache_dtype``.
+    ``operand_dtype``: as for ``forward``.
     """
     T = len(prompt)
     causal = torch.tril(torch.ones(T, T, dtype=torch.bool))
     s = {"tokens": [int(t) for t in prompt], "pos": torch.arange(T, dtype=torch.int64),
          "visible_tree": causal, "prefix_k": None, "prefix_v": None}
-    logits, ks, vs = forward(cfg, W, [s])
+    logits, ks, vs = forward(cfg, W, [s], operand_dtype)
     return ks[0].to(cache_dtype), vs[0].to(cache_dtype), logits

@@ -29,6 +29,30 @@ MUTATIONS = {
     "mask not applied": ('s = s.masked_fill(~visible, float("-inf"))', "s = s"),
     "deepest-node tie toward higher index": ("depth[i] > depth[best]", "depth[i] >= depth[best]"),
     "acceptance ignores the parent": ("accepted[i] = accepted[p] and", "accepted[i] ="),
+    # rounding points of the bf16-operand mode
+    "bf16: attention norm output not rounded": (
+        'h = rnd(rms_norm(x, _f64(lw["attn_norm"]), cfg.rms_eps))',
+        'h = rms_norm(x, _f64(lw["attn_norm"]), cfg.rms_eps)'),
+    "bf16: v not rounded": ('v = rnd((h @ _f64(lw["wv"]).T).view(N, nkv, d))',
+                            'v = (h @ _f64(lw["wv"]).T).view(N, nkv, d)'),
+    "bf16: q not rounded": ("q = rnd(rope(q, cos, sin))", "q = rope(q, cos, sin)"),
+    "bf16: k rounded before the rotation": (
+        ['k = (h @ _f64(lw["wk"]).T).view(N, nkv, d)', "k = rnd(rope(k, cos, sin))"],
+        ['k = rnd((h @ _f64(lw["wk"]).T).view(N, nkv, d))', "k = rope(k, cos, sin)"]),
+    "bf16: softmax numerators not rounded": ("(rnd(e) @ v_all[kv])", "(e @ v_all[kv])"),
+    "bf16: normalised weights rounded": (
+        "(rnd(e) @ v_all[kv]) / e.sum(dim=-1, keepdim=True)",
+        "rnd(e / e.sum(dim=-1, keepdim=True)) @ v_all[kv]"),
+    "bf16: attention output not rounded": ("x = x + rnd(o.reshape(N, nq * d)) @",
+                                           "x = x + o.reshape(N, nq * d) @"),
+    "bf16: ffn norm output not rounded": (
+        'h2 = rnd(rms_norm(x, _f64(lw["ffn_norm"]), cfg.rms_eps))',
+        'h2 = rms_norm(x, _f64(lw["ffn_norm"]), cfg.rms_eps)'),
+    "bf16: activation not rounded": ("x = x + rnd(torch.nn.functional.silu(gate) * up) @",
+                                     "x = x + (torch.nn.functional.silu(gate) * up) @"),
+    "bf16: final norm output not rounded": (
+        'hf = rnd(rms_norm(x, _f64(W["final_norm"]), cfg.rms_eps))',
+        'hf = rms_norm(x, _f64(W["final_norm"]), cfg.rms_eps)'),
 }
 
 
@@ -40,8 +64,10 @@ def test_pins_catch_planted_mistake(tmp_path, name):
         shutil.copytree(os.path.join(ROOT, d), tmp_path / d,
                         ignore=shutil.ignore_patterns("__pycache__", "golden"))
     src = (tmp_path / "oracle" / "verify.py").read_text()
-    assert before in src, name
-    (tmp_path / "oracle" / "verify.py").write_text(src.replace(before, after))
+    for b, a in zip(*((before, after) if isinstance(before, list) else ([before], [after]))):
+        assert src.count(b) == 1, (name, b)
+        src = src.replace(b, a)
+    (tmp_path / "oracle" / "verify.py").write_text(src)
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
                         "tests/test_oracle_pins.py"], cwd=tmp_path, capture_output=True,
                        text=True, timeout=600)

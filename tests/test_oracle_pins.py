@@ -10,7 +10,12 @@
   Section 2.2);
 * special cases: a one-node tree is one autoregressive step, a star tree is
   a set of independent one-token continuations, nkv = nq is ordinary
-  multi-head attention, relabelling the nodes permutes the results.
+  multi-head attention, relabelling the nodes permutes the results;
+* the bf16-operand mode (the ideal bf16 computation that sets the tolerance
+  of full-depth GPU comparisons) against the same independent decoder with
+  every bf16 storage point rounded by hooks on its own modules: equal to
+  rounding order, while leaving out any one rounding point moves the logits
+  by more than 1e-3.
 
 All CPU; no GPU needed.
 """
@@ -23,7 +28,7 @@ import torch
 
 import oracle
 import workload as wl
-from tests.hf_ref import hf_greedy, hf_logits, hf_model
+from tests.hf_ref import STORAGE_POINTS, bf16_storage, hf_greedy, hf_logits, hf_model, hf_model_f64
 
 PIN = wl.ModelConfig(n_layers=2, hidden=64, n_heads=4, n_kv_heads=2, head_dim=16, ffn=128,
                      vocab=97, rope_theta=1e4, rms_eps=1e-5)
@@ -361,3 +366,77 @@ def test_verify_leaves_prefix_untouched(pin_setup):
     path = torch.tensor(r["path"][0])
     assert torch.equal(ks[0][:, :, 9:], r["tree_k"][0][:, :, path])
     assert lens == [9 + r["accepted_len"][0] + 1]
+
+
+# ---------------------------------------------------------------------------
+# the bf16-operand mode
+# ---------------------------------------------------------------------------
+
+def bf16_weights(W):
+    """The same weights rounded to bf16 values (as the GPU holds them)."""
+    r = lambda t: t.to(torch.bfloat16).to(torch.float64)   # noqa: E731
+    return {"tok_embed": r(W["tok_embed"]), "final_norm": r(W["final_norm"]),
+            "lm_head": r(W["lm_head"]),
+            "layers": [{k: r(v) for k, v in lw.items()} for lw in W["layers"]]}
+
+
+@pytest.fixture(scope="module")
+def pin_setup_f64():
+    W = bf16_weights(pin_weights(PIN, 21))
+    return W, hf_model_f64(PIN, W)
+
+
+def bf16_case(seed):
+    rng = np.random.default_rng(300 + seed)
+    prompt = wl.random_tokens(rng, 9, PIN.vocab)
+    parents = wl.recursive_tree(rng, 18, 6, 3)
+    tokens = wl.random_tokens(rng, len(parents), PIN.vocab)
+    return prompt, tokens, parents
+
+
+def test_exact_mode_matches_float64_decoder(pin_setup_f64):
+    """With RMSNorm, rotary tables and softmax in float64 the decoder and the
+    exact oracle agree to rounding order."""
+    W, model = pin_setup_f64
+    prompt, tokens, parents = bf16_case(0)
+    r = run_verify(PIN, W, prompt, (tokens, parents))
+    with bf16_storage(model, skip=STORAGE_POINTS):
+        for i in range(len(parents)):
+            ref = hf_logits(model, prompt + branch_tokens(tokens, parents, i))[-1]
+            assert (r["logits"][i] - ref).abs().max().item() < 1e-12 * max(1.0, ref.abs().max().item())
+
+
+def test_operand_mode_none_is_the_exact_path(pin_setup_f64):
+    W, _ = pin_setup_f64
+    prompt, tokens, parents = bf16_case(1)
+    pk, pv, _ = oracle.prefill(PIN, W, prompt, cache_dtype=torch.float64)
+    a = oracle.verify(PIN, W, [pk], [pv], [len(prompt)], [(tokens, parents)])
+    for od in (None, torch.float64):
+        b = oracle.verify(PIN, W, [pk], [pv], [len(prompt)], [(tokens, parents)], operand_dtype=od)
+        assert torch.equal(a["logits"], b["logits"])
+        assert torch.equal(a["tree_k"][0], b["tree_k"][0]) and torch.equal(a["tree_v"][0], b["tree_v"][0])
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_bf16_operand_mode_matches_rounded_decoder(pin_setup_f64, seed):
+    """Every node's bf16-mode logits equal its branch decoded on its own by
+    the decoder with the bf16 storage points rounded; leaving out any single
+    rounding point (in the decoder) moves some logit by more than 1e-3, so an
+    oracle that missed one would fail here."""
+    W, model = pin_setup_f64
+    prompt, tokens, parents = bf16_case(seed)
+    bf = torch.bfloat16
+    pk, pv, _ = oracle.prefill(PIN, W, prompt, cache_dtype=bf, operand_dtype=bf)
+    r = oracle.verify(PIN, W, [pk], [pv], [len(prompt)], [(tokens, parents)], operand_dtype=bf)
+    branches = [prompt + branch_tokens(tokens, parents, i) for i in range(len(parents))]
+    with bf16_storage(model):
+        ref = torch.stack([hf_logits(model, br)[-1] for br in branches])
+    scale = ref.abs().max().item()
+    assert (r["logits"] - ref).abs().max().item() < 1e-12 * scale
+    # the K/V the bf16 mode stores are bf16 values
+    assert torch.equal(r["tree_k"][0], r["tree_k"][0].to(bf).to(torch.float64))
+    assert torch.equal(r["tree_v"][0], r["tree_v"][0].to(bf).to(torch.float64))
+    for point in STORAGE_POINTS:
+        with bf16_storage(model, skip=(point,)):
+            alt = torch.stack([hf_logits(model, br)[-1] for br in branches])
+        assert (r["logits"] - alt).abs().max().item() > 1e-3, point
