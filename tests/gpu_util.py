@@ -2,22 +2,31 @@
 running the oracle on the same bits, and the comparison rules.
 
 Comparison rules (tolerance of the verify step on bf16 logits):
-* shallow models (2 layers): |z_gpu - z_oracle| <= ATOL + RTOL * |z_oracle|
-  element-wise against the exact oracle;
-* full-depth models: bf16 storage noise alone moves deep random-weight
-  logits further than that (an ideal bf16-operand computation of the oracle
-  misses it too), so the GPU's error against the exact oracle must stay
-  inside the envelope of that ideal bf16 computation's error: mean, 99.9th
-  percentile and per-node relative L2 error at most ENV_FACTOR times the
+* shallow models (2 layers) at hidden <= 2048: |z_gpu - z_oracle| <= ATOL +
+  RTOL * |z_oracle| element-wise against the exact oracle;
+* deeper or wider models: bf16 storage noise alone moves random-weight
+  logits further than that (the oracle's ideal bf16-operand computation,
+  pinned on the CPU against an independently rounded decoder, misses it
+  too), so the GPU's error against the exact oracle must stay inside the
+  envelope of that ideal computation's error: mean, 99.9th percentile,
+  per-node relative L2 and maximum error at most ENV_FACTOR times the
   ideal's (plus a small floor);
-* greedy tokens: equal, or "tie-excused" where the oracle's logit of the
-  GPU's choice is within the comparison's tolerance of the oracle's maximum
-  (ATOL for shallow models; twice the GPU's largest logit error at depth,
-  the most by which two logits can swap order);
+* greedy tokens: equal, or "tie-excused" where the exact oracle's logit of
+  the GPU's choice is within the tie tolerance of the oracle's maximum.  The
+  tie tolerance is ATOL for the element-wise rule; under the envelope it is
+  twice the largest error the envelope allows, ENV_FACTOR times the ideal
+  computation's maximum error (plus the floor): never the GPU's own error.
+  The excused count is bounded by that of the ideal computation
+  (EXCUSE_FACTOR times its disagreements with the exact oracle, plus
+  EXCUSE_SLACK);
 * acceptance: bit-exact against the oracle's acceptance run on the GPU's own
-  greedy tokens, and end to end equal to the oracle wherever the two agree
-  on every greedy token of the sample;
+  greedy tokens for every sample, and end to end equal to the oracle's for
+  every checked sample with no excused disagreement at a node that either
+  side accepts (only those nodes' greedy tokens decide acceptance);
 * depth, positions, ancestor sets, compacted KV positions: bit-exact.
+
+Every comparison appends one summary line to PARITY_LOG; the test session
+prints them at its end.
 """
 
 import dataclasses
@@ -34,6 +43,17 @@ import workload as wl
 
 ATOL, RTOL = 3e-2, 2e-2
 ENV_FACTOR = 1.5
+ENV_FLOOR = {"mean": 1e-3, "q999": 5e-3, "rowrel": 1e-3, "max": 5e-3}
+EXCUSE_FACTOR, EXCUSE_SLACK = 3, 4
+
+PARITY_LOG = []
+
+
+def log_parity(line):
+    import os
+    test = os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0].split("::")[-1]
+    PARITY_LOG.append(f"{test}: {line}")
+    say("  parity " + line)
 
 
 def say(*a):
@@ -56,13 +76,15 @@ def prefix_for_oracle(ver, ids, lens):
     return ks, vs
 
 
-def run_gpu(ver, ids, trees, lens, logits=True):
-    """One verify through the C ABI with debug dumps; returns host results."""
+def run_gpu(ver, ids, trees, lens, logits=True, rows=None):
+    """One verify through the C ABI with debug dumps; returns host results
+    (only the logits of ``rows``, when given)."""
     n = sum(len(t[0]) for t in trees)
     dbg = ver.debug_buffers(n, logits=logits)
     acc, nxt, nodes = ver.verify(ids, trees, lens, debug=dbg)
     torch.cuda.synchronize()
-    out = {k: v.cpu() for k, v in dbg.items()}
+    out = {k: (v[rows] if k == "logits" and rows is not None else v).cpu() for k, v in dbg.items()}
+    del dbg
     out["accepted_len"] = acc.cpu().tolist()
     out["next_token"] = nxt.cpu().tolist()
     out["nodes"] = nodes.cpu()
@@ -86,56 +108,81 @@ def check_logits(z_gpu, z_or, what=""):
     say(f"  logits {what}: max_abs {err.max().item():.3e} max_rel {rel:.3e} "
         f"violations {int(bad.sum())}/{bad.numel()}")
     assert not bad.any(), f"{what}: {int(bad.sum())} logits outside tolerance, max err {err.max()}"
+    return {"rule": "element-wise", "max_abs": err.max().item(), "max_rel": rel,
+            "strict": 0.0, "tie_tol": ATOL, "ideal_flips": None}
 
 
 def check_envelope(z_gpu, z_or, z_ideal, what=""):
     """Full-depth rule: the GPU's deviation from the exact oracle is no larger
-    than an ideal bf16-operand computation's, within ENV_FACTOR.  Returns the
-    tie tolerance (twice the GPU's largest error)."""
+    than the ideal bf16-operand computation's, within ENV_FACTOR (plus
+    ENV_FLOOR), in mean, 99.9th percentile, per-node relative L2 and maximum.
+    Returns the comparison's statistics and its tie tolerance, which comes
+    from the ideal computation only."""
     z_or = z_or.to(torch.float64)
     e_gpu = (z_gpu.to(torch.float64) - z_or).abs()
     e_ref = (z_ideal.to(torch.float64) - z_or).abs()
-    rr = lambda e: (e.norm(dim=-1) / z_or.norm(dim=-1)).max().item()
-    q = lambda e: torch.quantile(e.flatten()[:: max(1, e.numel() // 4_000_000)].float(), 0.999).item()
+    rr = lambda e: (e.norm(dim=-1) / z_or.norm(dim=-1)).max().item()     # noqa: E731
+    q = lambda e: torch.quantile(e.flatten()[:: max(1, e.numel() // 4_000_000)].float(),  # noqa: E731
+                                 0.999).item()
     stats = {"mean": (e_gpu.mean().item(), e_ref.mean().item()),
              "q999": (q(e_gpu), q(e_ref)), "rowrel": (rr(e_gpu), rr(e_ref)),
              "max": (e_gpu.max().item(), e_ref.max().item())}
-    strict = (e_gpu > ATOL + RTOL * z_or.abs()).float().mean().item()
+    bound = ATOL + RTOL * z_or.abs()
+    strict = (e_gpu > bound).float().mean().item()
+    strict_ideal = (e_ref > bound).float().mean().item()
     say(f"  logits {what} (gpu, ideal bf16): " +
         " ".join(f"{k} {a:.3e}/{b:.3e}" for k, (a, b) in stats.items()) +
-        f"; strict-rule violations {strict:.4%}")
-    floor = {"mean": 1e-3, "q999": 5e-3, "rowrel": 1e-3}
-    for k, f in floor.items():
+        f"; strict-rule violations {strict:.4%} / {strict_ideal:.4%}")
+    for k, f in ENV_FLOOR.items():
         a, b = stats[k]
         assert a <= ENV_FACTOR * b + f, f"{what}: {k} error {a:.4e} exceeds envelope {b:.4e}"
-    return 2 * stats["max"][0]
+    g_or = torch.argmax(z_or, dim=-1)
+    ideal_flips = int((torch.argmax(z_ideal.to(torch.float64), dim=-1) != g_or).sum())
+    tie_tol = 2 * (ENV_FACTOR * stats["max"][1] + ENV_FLOOR["max"])
+    return {"rule": "envelope", "max_abs": stats["max"][0], "ideal_max_abs": stats["max"][1],
+            "mean": stats["mean"], "strict": strict, "strict_ideal": strict_ideal,
+            "tie_tol": tie_tol, "ideal_flips": ideal_flips}
 
 
 def check_argmax(g_gpu, z_or, tol=ATOL):
-    """Returns the number of tie-excused disagreements; fails on others."""
+    """Returns the rows of tie-excused disagreements; fails on any other."""
     g_or = torch.argmax(z_or, dim=-1)
-    excused = 0
+    excused = []
     for i in range(len(g_gpu)):
         if int(g_gpu[i]) != int(g_or[i]):
             row = z_or[i]
             assert row[int(g_gpu[i])] >= row.max() - tol, \
                 f"node {i}: gpu {int(g_gpu[i])} vs oracle {int(g_or[i])}, margin " \
-                f"{(row.max() - row[int(g_gpu[i])]).item():.4f}"
-            excused += 1
+                f"{(row.max() - row[int(g_gpu[i])]).item():.4f} beyond the tie tolerance {tol:.4f}"
+            excused.append(i)
     return excused
 
 
+def accepted_set(tokens, parents, g):
+    """Nodes accepted under greedy tokens g (the root always)."""
+    acc = [True] + [False] * (len(tokens) - 1)
+    for i in range(1, len(tokens)):
+        acc[i] = acc[parents[i]] and int(tokens[i]) == int(g[parents[i]])
+    return {i for i in range(len(tokens)) if acc[i]}
+
+
 def check_sample_acceptance(tokens, parents, g_gpu_b, gpu_len, gpu_next, gpu_nodes,
-                            or_res=None, b=None, g_or_b=None):
+                            or_res=None, b=None, g_or_b=None, excused_nodes=()):
     """Bit-exact: the oracle's acceptance on the GPU's greedy tokens equals the
-    GPU's; and equal to the oracle's own result when all greedy tokens agree."""
+    GPU's; and, when no excused node is accepted by either side, equal to the
+    oracle's own result.  Returns True when the end-to-end comparison ran."""
     a, nx, path = oracle.greedy_accept(tokens, parents, g_gpu_b)
     assert (gpu_len, gpu_next) == (a, nx)
     nodes = gpu_nodes.tolist()
     assert nodes[:a + 1] == path and all(x == -1 for x in nodes[a + 1:])
-    if or_res is not None and list(g_gpu_b) == list(g_or_b):
-        assert or_res["accepted_len"][b] == a and or_res["path"][b] == path
-        assert or_res["next_token"][b] == nx
+    if or_res is None:
+        return False
+    deciding = accepted_set(tokens, parents, g_gpu_b) | accepted_set(tokens, parents, g_or_b)
+    if deciding & set(excused_nodes):
+        return False
+    assert or_res["accepted_len"][b] == a and or_res["path"][b] == path
+    assert or_res["next_token"][b] == nx
+    return True
 
 
 def check_meta(trees, lens, out):
@@ -154,43 +201,58 @@ def full_check(cfg, W_cpu, ver, ids, trees, lens, check_ids=None, envelope=False
     """GPU verify of the whole batch; oracle on samples ``check_ids`` (all by
     default).  ``envelope`` selects the full-depth rule.  Returns (gpu
     result, oracle result, excused count)."""
+    offs = split_rows(trees)
+    if check_ids is None:
+        check_ids = list(range(len(trees)))
+    rows = torch.cat([torch.arange(offs[b], offs[b + 1]) for b in check_ids])
     t0 = time.time()
-    out = run_gpu(ver, ids, trees, lens)
+    out = run_gpu(ver, ids, trees, lens, rows=rows)
     say(f"  gpu verify done ({time.time() - t0:.1f}s)")
     check_meta(trees, lens, out)
-    offs = split_rows(trees)
     g_gpu = out["argmax"].tolist()
     # acceptance on the GPU's own greedy tokens: every sample, bit-exact
     for b, (tokens, parents) in enumerate(trees):
         check_sample_acceptance(tokens, parents, g_gpu[offs[b]:offs[b + 1]],
                                 out["accepted_len"][b], out["next_token"][b], out["nodes"][b])
-    if check_ids is None:
-        check_ids = list(range(len(trees)))
     pk, pv = prefix_for_oracle(ver, [ids[b] for b in check_ids], [lens[b] for b in check_ids])
     t0 = time.time()
     r = oracle.verify(cfg, W_cpu, pk, pv, [lens[b] for b in check_ids],
                       [trees[b] for b in check_ids])
     say(f"  oracle on {len(check_ids)} samples done ({time.time() - t0:.1f}s)")
-    rows = torch.cat([torch.arange(offs[b], offs[b + 1]) for b in check_ids])
     if envelope:
         t0 = time.time()
         ri = oracle.verify(cfg, W_cpu, pk, pv, [lens[b] for b in check_ids],
                            [trees[b] for b in check_ids], operand_dtype=torch.bfloat16)
         say(f"  ideal bf16-operand oracle done ({time.time() - t0:.1f}s)")
-        tol = check_envelope(out["logits"][rows], r["logits"], ri["logits"], f"{len(rows)} rows")
+        st = check_envelope(out["logits"], r["logits"], ri["logits"], f"{len(rows)} rows")
+        del ri
     else:
-        check_logits(out["logits"][rows], r["logits"], f"{len(rows)} rows")
-        tol = ATOL
-    excused = check_argmax(out["argmax"][rows], r["logits"], tol)
+        st = check_logits(out["logits"], r["logits"], f"{len(rows)} rows")
+    excused = check_argmax(out["argmax"][rows], r["logits"], st["tie_tol"])
+    if st["ideal_flips"] is not None:
+        assert len(excused) <= EXCUSE_FACTOR * st["ideal_flips"] + EXCUSE_SLACK, \
+            f"{len(excused)} excused disagreements, the ideal bf16 computation has {st['ideal_flips']}"
     roffs = split_rows([trees[b] for b in check_ids])
     g_or = r["argmax"].tolist()
+    e2e = 0
     for j, b in enumerate(check_ids):
         tokens, parents = trees[b]
-        check_sample_acceptance(tokens, parents, g_gpu[offs[b]:offs[b + 1]],
-                                out["accepted_len"][b], out["next_token"][b], out["nodes"][b],
-                                r, j, g_or[roffs[j]:roffs[j + 1]])
-    say(f"  tie-excused argmax disagreements: {excused}")
-    return out, r, excused
+        exc_local = [i - roffs[j] for i in excused if roffs[j] <= i < roffs[j + 1]]
+        e2e += check_sample_acceptance(tokens, parents, g_gpu[offs[b]:offs[b + 1]],
+                                       out["accepted_len"][b], out["next_token"][b],
+                                       out["nodes"][b], r, j, g_or[roffs[j]:roffs[j + 1]],
+                                       exc_local)
+    line = (f"L{cfg.n_layers} H{cfg.hidden} rows {len(rows)} {st['rule']}: "
+            f"max_abs {st['max_abs']:.3g}")
+    if st["rule"] == "envelope":
+        line += (f" (ideal {st['ideal_max_abs']:.3g}), mean {st['mean'][0]:.3g} "
+                 f"(ideal {st['mean'][1]:.3g}), strict-rule outside {st['strict']:.3%} "
+                 f"(ideal {st['strict_ideal']:.3%})")
+    line += (f", tie_tol {st['tie_tol']:.3g}, excused {len(excused)}"
+             + (f" (ideal flips {st['ideal_flips']})" if st["ideal_flips"] is not None else "")
+             + f", end-to-end {e2e}/{len(check_ids)} samples")
+    log_parity(line)
+    return out, r, len(excused)
 
 
 def check_tree_kv(cfg, ver, ids, trees, lens, r, check_ids, layers=None):
@@ -268,3 +330,20 @@ def oracle_greedy_fn(cfg, W_cpu, ver, ids, lens):
         return [g[offs[b]:offs[b + 1]] for b in range(len(trees))]
 
     return fn
+
+
+def sweep_setup(cfg, W_dev, seed=4000):
+    """The launch configuration the strategy-cost sweep times: one pool of the
+    256 sweep samples (lognormal committed lengths, room for a 64-node tree
+    each) and one verifier sized for 256 samples x 64 nodes; a batch-B cell
+    takes the first B samples."""
+    lens_all = [int(x) for x in wl.sweep_lengths(seed)]
+    caps = [S + max(wl.SWEEP_BUDGETS) for S in lens_all]
+    max_b = max(wl.SWEEP_BATCHES)
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=max_b, max_tokens=max_b * max(wl.SWEEP_BUDGETS))
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    for b, S in enumerate(lens_all):
+        k, v = ver.kv.sample_view(b)
+        wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    return ver

@@ -7,6 +7,8 @@ exact because samples never interact in a verify step.
 """
 
 
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -17,7 +19,7 @@ import workload as wl
 from tests.gpu_util import (ATOL, check_argmax, check_logits, check_sample_acceptance,
                             check_tree_kv, cpu_weights, device_setup, full_check,
                             oracle_greedy_fn, prefix_for_oracle, release, run_gpu, say, shallow,
-                            split_rows, tiny_setup)
+                            split_rows, sweep_setup, tiny_setup)
 
 pytestmark = pytest.mark.gpu
 
@@ -273,3 +275,116 @@ def test_llama8b_tail_phase_sampled(w8b):
                              envelope=True)
     check_tree_kv(w.cfg, ver, ids, w.trees, lens, r, check, layers=1)
     release(ver)
+
+
+# ---------------------------------------------------------------------------
+# the strategy-cost sweep's large cells, in the sweep's launch configuration
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("batch,budget", [(64, 64), (256, 32)])
+def test_sweep_cell_two_layer(batch, budget):
+    """4,096 and 8,192 node rows: the 256 x 256 tiles of the q/k/v product
+    (rotary + K/V-write epilogue) and of the residual products (split-free
+    epilogue), every GEMM and attention kernel the sweep runs at these
+    sizes, on a 2-layer 8B-shape model; the checked samples' deepest branch
+    follows the oracle's greedy choice so that acceptance is exercised."""
+    cfg = dataclasses.replace(wl.LLAMA_8B, n_layers=2)
+    W_dev = wl.make_weights(cfg, 70 + budget, device="cuda")
+    W_cpu = cpu_weights(W_dev)
+    ver = sweep_setup(cfg, W_dev)
+    w = wl.sweep_workload(batch, budget)
+    w.cfg = cfg
+    ids, lens = list(range(batch)), [int(x) for x in w.seq_lens]
+    check = sorted({int(np.argmax(lens)), batch // 2 + 1})
+    say(f"{w.name}: 2-layer 8B shape, {w.n_tokens} nodes, checked samples {check}")
+    sub = [w.trees[b] for b in check]
+    wl.follow_greedy(sub, [w.branches[b] for b in check], 1.0,
+                     oracle_greedy_fn(cfg, W_cpu, ver, check, [lens[b] for b in check]),
+                     np.random.default_rng(budget))
+    out, r, exc = full_check(cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check, envelope=True)
+    check_tree_kv(cfg, ver, ids, w.trees, lens, r, check, layers=1)
+    assert any(out["accepted_len"][b] > 0 for b in check)
+    release(ver, W_dev)
+
+
+@pytest.mark.parametrize("batch,budget", [(64, 32), (256, 64)])
+def test_sweep_cell_full_depth(w8b, batch, budget):
+    """2,048 and 16,384 node rows at 32 layers, whole batch on the GPU in the
+    sweep's launch configuration; the oracle checks two samples (the longest
+    committed prefix and one from the middle), exact since samples never
+    interact."""
+    W_dev, W_cpu = w8b
+    ver = sweep_setup(wl.LLAMA_8B, W_dev)
+    w = wl.sweep_workload(batch, budget)
+    ids, lens = list(range(batch)), [int(x) for x in w.seq_lens]
+    check = sorted({int(np.argmax(lens)), batch // 2 + 1})
+    say(f"{w.name}: 32-layer 8B shape, {w.n_tokens} nodes, checked samples {check} "
+        f"(KV {[lens[b] for b in check]})")
+    out, r, exc = full_check(w.cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check,
+                             envelope=True)
+    check_tree_kv(w.cfg, ver, ids, w.trees, lens, r, check, layers=1)
+    release(ver)
+
+
+def test_llama1b_multistep_matches_greedy_decoding():
+    """Verify + commit rounds at the 16-layer 1B shape with chain drafts (the
+    oracle's greedy stream, each draft token replaced at random with p = 0.3)
+    reproduce the oracle's plain greedy decoding token for token (lossless,
+    Section 2.2), up to a divergence at a near-tie of the exact logits: the
+    tie tolerance of each position is the envelope's, from the ideal
+    bf16-operand computation of that decoding step."""
+    from tests.gpu_util import ENV_FACTOR, ENV_FLOOR
+    cfg = wl.LLAMA_1B
+    say("llama-1B shape multi-step: 1 sample, committed KV 700, chain drafts of 4")
+    W_dev = wl.make_weights(cfg, 1100, device="cuda")
+    W64 = {"tok_embed": W_dev["tok_embed"].cpu().double(),
+           "final_norm": W_dev["final_norm"].cpu().double(),
+           "lm_head": W_dev["lm_head"].cpu().double(),
+           "layers": [{k: v.cpu().double() for k, v in lw.items()} for lw in W_dev["layers"]]}
+    S0 = 700
+    ver = sv.Verifier(cfg, W_dev, [S0 + 96], max_batch=1, max_tokens=64)
+    gen = torch.Generator(device="cuda").manual_seed(1100)
+    k, v = ver.kv.sample_view(0)
+    wl.fill_prefix_kv(k, v, S0, wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    pk, pv = prefix_for_oracle(ver, [0], [S0])
+    rng = np.random.default_rng(1100)
+    root = int(rng.integers(cfg.vocab))
+    ks, vs, lens = pk, pv, [S0]
+    want, zs, tols, cur = [root], [], [], root
+    for _ in range(26):
+        r = oracle.verify(cfg, W64, ks, vs, lens, [([cur], [-1])])
+        ri = oracle.verify(cfg, W64, ks, vs, lens, [([cur], [-1])], operand_dtype=torch.bfloat16)
+        zs.append(r["logits"][0])
+        tols.append(2 * (ENV_FACTOR * (ri["logits"][0] - r["logits"][0]).abs().max().item()
+                         + ENV_FLOOR["max"]))
+        cur = r["next_token"][0]
+        want.append(cur)
+        ks, vs, lens = oracle.commit(ks, vs, lens, r)
+    say(f"  oracle greedy stream done, tie tolerances {min(tols):.3g}..{max(tols):.3g}")
+    got, S, steps, diverged = [root], S0, 0, False
+    while len(got) < 24 and not diverged:
+        n0 = len(got)
+        draft = [got[-1]] + [want[n0 + j] if rng.random() > 0.3 else int(rng.integers(cfg.vocab))
+                             for j in range(3)]
+        acc, nxt, nodes = ver.verify([0], [(draft, wl.chain_tree(4))], [S])
+        new_len = ver.commit([0], [S])
+        torch.cuda.synchronize()
+        a, n = int(acc[0]), int(nxt[0])
+        assert nodes[0, :a + 1].tolist() == list(range(a + 1))
+        for t in draft[1:a + 1] + [n]:
+            j = len(got)
+            if t != want[j]:
+                z = zs[j - 1]
+                assert z[t] >= z.max() - tols[j - 1], f"stream diverges at {j} without a near-tie"
+                say(f"  tie-excused divergence at token {j} (margin "
+                    f"{(z.max() - z[t]).item():.3g} < {tols[j - 1]:.3g})")
+                diverged = True
+                break
+            got.append(t)
+        S += a + 1
+        assert int(new_len[0]) == S
+        steps += 1
+    say(f"  {len(got)} tokens equal to greedy decoding in {steps} steps")
+    assert len(got) >= 24 or diverged
+    release(ver, W_dev)
