@@ -209,6 +209,32 @@ int spec_verify_sampled(const spec_model_config* cfg, const spec_weights* w, spe
                         const spec_sampling* samp, int32_t* accepted_len, int32_t* next_token,
                         int32_t* accepted_nodes, const spec_debug* dbg);
 
+/* ---- Verify without a caller workspace ---------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * spec_verify with its workspace taken from a static device array of
+ * SPEC_NOALLOC_SCRATCH_BYTES, one per device, held by the library from the
+ * first call on that device until the process ends.  Arguments, outputs, KV
+ * effect and results are spec_verify's (bitwise: the same plan and kernels),
+ * without workspace and ws_bytes.  The call makes no device or pinned host
+ * allocation; its per-call descriptors go to the device from pageable host
+ * memory (hipMemcpyAsync, which may block the calling thread until the copy
+ * is done).  Returns SPEC_ERR_WORKSPACE, before enqueueing anything, when
+ * spec_workspace_bytes(cfg, batch, N) exceeds SPEC_NOALLOC_SCRATCH_BYTES (at
+ * the Llama-3-8B shape, 128 samples with 1024 tree nodes in total fit).
+ * Every call on one device shares that device's array and leaves its
+ * contents behind: calls that overlap on one device (two streams, two
+ * threads) race and must be serialised by the caller.  The calling thread's
+ * current device must be the stream's; SPEC_ERR_HIP if the array's address
+ * cannot be looked up on it. */
+#define SPEC_NOALLOC_SCRATCH_BYTES ((size_t)320 << 20)
+
+int spec_verify_noalloc(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv,
+                        int32_t batch, const int32_t* sample_ids, const int32_t* tree_offsets,
+                        const int32_t* tree_tokens, const int32_t* tree_parents,
+                        const int32_t* seq_lens, void* stream, int32_t* accepted_len,
+                        int32_t* next_token, int32_t* accepted_nodes, const spec_debug* dbg);
+
 /* Commit the accepted branches of the preceding spec_verify (same batch,
  * sample_ids and seq_lens, same stream): the K/V of node accepted_nodes[b][d]
  * moves to position S_b + d for d = 1..accepted_len[b] (all layers, K and

@@ -28,7 +28,8 @@ EXPORTS = ("spec_kv_bytes", "spec_kv_alloc", "spec_kv_free", "spec_kv_sample_lay
            "spec_profile_begin", "spec_profile_end", "spec_kv_transfer_bytes", "spec_kv_pack",
            "spec_kv_unpack", "spec_cost_model_create", "spec_cost_model_free", "spec_cost_predict",
            "spec_cost_model_stats", "spec_select_draft_count", "spec_workspace_bytes_sampled",
-           "spec_verify_sampled")
+           "spec_verify_sampled", "spec_verify_noalloc")
+SPEC_NOALLOC_SCRATCH_BYTES = 320 << 20
 
 
 class SpecError(RuntimeError):
@@ -98,6 +99,9 @@ def lib():
                                       c_int32, i32p, i32p, i32p, i32p, i32p, c_void_p, c_size_t,
                                       c_void_p, POINTER(spec_sampling), c_void_p, c_void_p,
                                       c_void_p, POINTER(spec_debug)]
+    L.spec_verify_noalloc.argtypes = [POINTER(spec_model_config), POINTER(spec_weights),
+                                      c_void_p, c_int32, i32p, i32p, i32p, i32p, i32p, c_void_p,
+                                      c_void_p, c_void_p, c_void_p, POINTER(spec_debug)]
     L.spec_kv_transfer_bytes.argtypes = [c_void_p, c_int32, i32p, i32p]
     L.spec_kv_transfer_bytes.restype = c_size_t
     L.spec_kv_pack.argtypes = [c_void_p, c_int32, i32p, i32p, i32p, c_void_p, c_size_t, c_void_p]
@@ -116,7 +120,8 @@ def lib():
     for name in ("spec_kv_alloc", "spec_kv_free", "spec_kv_sample_layout", "spec_verify",
                  "spec_kv_commit", "spec_profile_begin", "spec_profile_end", "spec_kv_pack",
                  "spec_kv_unpack", "spec_cost_model_create", "spec_cost_model_free",
-                 "spec_cost_model_stats", "spec_select_draft_count", "spec_verify_sampled"):
+                 "spec_cost_model_stats", "spec_select_draft_count", "spec_verify_sampled",
+                 "spec_verify_noalloc"):
         getattr(L, name).restype = c_int32
     _lib = L
     return L
@@ -254,6 +259,26 @@ def spec_verify(cfg, weights: Weights, kv: KVPool, sample_ids, tree_offsets, tre
                              _ptr(workspace), workspace.numel() * workspace.element_size(),
                              _stream(stream), _ptr(accepted_len), _ptr(next_token),
                              _ptr(accepted_nodes), ctypes.byref(dbg) if dbg else None))
+
+
+def spec_verify_noalloc(cfg, weights: Weights, kv: KVPool, sample_ids, tree_offsets, tree_tokens,
+                        tree_parents, seq_lens, accepted_len, next_token, accepted_nodes,
+                        debug=None, stream=None):
+    """spec_verify with the library's static device scratch as workspace."""
+    c = make_config(cfg)
+    ids, p_ids = _i32(sample_ids)
+    offs, p_offs = _i32(tree_offsets)
+    toks, p_toks = _i32(tree_tokens)
+    pars, p_pars = _i32(tree_parents)
+    lens, p_lens = _i32(seq_lens)
+    dbg = None
+    if debug:
+        dbg = spec_debug(*[debug[k].data_ptr() if debug.get(k) is not None else None
+                           for k in ("logits", "argmax", "depth", "pos", "anc")])
+    _check(lib().spec_verify_noalloc(ctypes.byref(c), ctypes.byref(weights.struct), kv.handle,
+                                     len(ids), p_ids, p_offs, p_toks, p_pars, p_lens,
+                                     _stream(stream), _ptr(accepted_len), _ptr(next_token),
+                                     _ptr(accepted_nodes), ctypes.byref(dbg) if dbg else None))
 
 
 def spec_workspace_bytes_sampled(cfg, max_batch, max_tokens) -> int:

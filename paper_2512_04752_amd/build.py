@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libspecverify.so")
 BUILD = os.path.join(PKG, "_build")
 SOURCES = ["api.cpp", "gemm.hip", "attention.hip", "elementwise.hip", "migrate.hip",
-           "strategy.cpp", "sampling.hip"]
+           "strategy.cpp", "sampling.hip", "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-x", "hip", "-std=c++17", "-O3", "--offload-arch=gfx950", "-fPIC",

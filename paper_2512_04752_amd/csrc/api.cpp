@@ -301,11 +301,11 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
                 const int32_t* sample_ids, const int32_t* tree_offsets, const int32_t* tree_tokens,
                 const int32_t* tree_parents, const int32_t* seq_lens, void* workspace,
                 size_t ws_bytes, void* stream, const spec_sampling* samp, int32_t* accepted_len,
-                int32_t* next_token, int32_t* accepted_nodes, const spec_debug* dbg) {
-  g_err.clear();
+                int32_t* next_token, int32_t* accepted_nodes, const spec_debug* dbg,
+                bool noalloc = false) {
   // ---- validation (no side effects) ----
   if (!cfg || !w || !kv || !sample_ids || !tree_offsets || !tree_tokens || !tree_parents ||
-      !seq_lens || !workspace || !accepted_len || !next_token || !accepted_nodes)
+      !seq_lens || (!workspace && !noalloc) || !accepted_len || !next_token || !accepted_nodes)
     return fail(SPEC_ERR_INVALID, "null argument");
   std::string why;
   if (!config_ok(cfg, &why)) return fail(SPEC_ERR_UNSUPPORTED, "%s", why.c_str());
@@ -353,6 +353,15 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
   }
   const int N = tree_offsets[batch];
   const size_t need = ws_layout(cfg, batch, N, sampled).total;
+  if (noalloc && need > SPEC_NOALLOC_SCRATCH_BYTES)
+    return fail(SPEC_ERR_WORKSPACE,
+                "%d samples with %d tree nodes need %zu bytes of workspace, more than the %zu "
+                "bytes of spec_verify_noalloc's static scratch",
+                batch, N, need, (size_t)SPEC_NOALLOC_SCRATCH_BYTES);
+  if (noalloc) {
+    HIP_TRY(noalloc_scratch(&workspace), "static scratch lookup");
+    ws_bytes = SPEC_NOALLOC_SCRATCH_BYTES;
+  }
   if (ws_bytes < need) return fail(SPEC_ERR_WORKSPACE, "workspace %zu bytes, needs %zu", ws_bytes, need);
 
   // ---- planning ----
@@ -483,7 +492,11 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
   if (!wide4.empty()) memcpy(blob.data() + o_wide4, wide4.data(), wide4.size() * sizeof(AttnItem));
   if (!wide8.empty()) memcpy(blob.data() + o_wide8, wide8.data(), wide8.size() * sizeof(AttnItem));
   if (!comb.empty()) memcpy(blob.data() + o_comb, comb.data(), comb.size() * sizeof(CombineItem));
-  if (int rc = stage_upload(kv, blob.data(), blob_bytes, ws + ly.blob, s)) return rc;
+  if (noalloc)   // no pinned staging: a copy from pageable memory, done before the call returns
+    HIP_TRY(hipMemcpyAsync(ws + ly.blob, blob.data(), blob_bytes, hipMemcpyHostToDevice, s),
+            "upload");
+  else if (int rc = stage_upload(kv, blob.data(), blob_bytes, ws + ly.blob, s))
+    return rc;
 
   const SampleInfo* d_si = (const SampleInfo*)(ws + ly.blob + o_si);
   const int32_t* d_tok = (const int32_t*)(ws + ly.blob + o_tok);
@@ -641,6 +654,7 @@ SPEC_API int spec_verify(const spec_model_config* cfg, const spec_weights* w, sp
                          const int32_t* seq_lens, void* workspace, size_t ws_bytes, void* stream,
                          int32_t* accepted_len, int32_t* next_token, int32_t* accepted_nodes,
                          const spec_debug* dbg) {
+  g_err.clear();
   return verify_impl(cfg, w, kv, batch, sample_ids, tree_offsets, tree_tokens, tree_parents,
                      seq_lens, workspace, ws_bytes, stream, nullptr, accepted_len, next_token,
                      accepted_nodes, dbg);
@@ -661,10 +675,23 @@ SPEC_API int spec_verify_sampled(const spec_model_config* cfg, const spec_weight
                                  const spec_sampling* samp, int32_t* accepted_len,
                                  int32_t* next_token, int32_t* accepted_nodes,
                                  const spec_debug* dbg) {
+  g_err.clear();
   if (!samp) return fail(SPEC_ERR_INVALID, "null sampling parameters");
   return verify_impl(cfg, w, kv, batch, sample_ids, tree_offsets, tree_tokens, tree_parents,
                      seq_lens, workspace, ws_bytes, stream, samp, accepted_len, next_token,
                      accepted_nodes, dbg);
+}
+
+SPEC_API int spec_verify_noalloc(const spec_model_config* cfg, const spec_weights* w,
+                                 spec_kv* kv, int32_t batch, const int32_t* sample_ids,
+                                 const int32_t* tree_offsets, const int32_t* tree_tokens,
+                                 const int32_t* tree_parents, const int32_t* seq_lens,
+                                 void* stream, int32_t* accepted_len, int32_t* next_token,
+                                 int32_t* accepted_nodes, const spec_debug* dbg) {
+  g_err.clear();
+  return verify_impl(cfg, w, kv, batch, sample_ids, tree_offsets, tree_tokens, tree_parents,
+                     seq_lens, nullptr, 0, stream, nullptr, accepted_len, next_token,
+                     accepted_nodes, dbg, true);
 }
 
 SPEC_API int spec_kv_commit(spec_kv* kv, int32_t batch, const int32_t* sample_ids,

@@ -115,6 +115,8 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 int gemm_parts(int N, int M, int K);
 // Bytes of split-K partial storage launch_gemm may use through GemmArgs::partial.
 size_t gemm_partial_bytes();
+// Device address of the current device's static scratch (noalloc.hip).
+hipError_t noalloc_scratch(void** out);
 
 struct AttnArgs {
   const bf16* q;            // [N][n_heads*head_dim]

@@ -57,6 +57,16 @@ class Verifier:
                       self.accepted_nodes, debug=debug, stream=stream)
         return self.accepted_len[:b], self.next_token[:b], self.accepted_nodes[:b]
 
+    def verify_noalloc(self, sample_ids, trees, seq_lens, debug=None, stream=None, flat=None):
+        """verify() on the library's static device scratch instead of this
+        session's workspace (spec_verify_noalloc)."""
+        offsets, tokens, parents = flat if flat is not None else flatten_trees(trees)
+        b = len(sample_ids)
+        B.spec_verify_noalloc(self.cfg, self.weights, self.kv, sample_ids, offsets, tokens,
+                              parents, seq_lens, self.accepted_len, self.next_token,
+                              self.accepted_nodes, debug=debug, stream=stream)
+        return self.accepted_len[:b], self.next_token[:b], self.accepted_nodes[:b]
+
     def verify_sampled(self, sample_ids, trees, seq_lens, temperature, eos_token=-1,
                        draft_probs=None, uniforms=None, debug=None, stream=None, flat=None):
         """Enqueue one verify step with speculative-sampling acceptance."""

@@ -291,3 +291,31 @@ def test_sampled_workspace_beyond_4gib():
     4 GiB for its fp32 logits alone)."""
     n = sv.spec_workspace_bytes_sampled(wl.LLAMA_8B, 512, 16384)
     assert n > 16384 * wl.LLAMA_8B.vocab * 4 > 1 << 32
+
+
+def test_noalloc_rejects_calls_beyond_its_scratch():
+    """spec_verify_noalloc refuses, before any device work, a call whose
+    workspace would exceed the static scratch, and validates like
+    spec_verify."""
+    cfg = wl.LLAMA_8B
+    caps = [4096] * 256
+    f = FakeVerify(cfg, caps)
+    try:
+        def call(ids, trees, lens):
+            offs, toks, pars = sv.flatten_trees(trees)
+            i = lambda a: B._i32(a)   # noqa: E731
+            (_, p1), (_, p2), (_, p3), (_, p4), (_, p5) = (i(ids), i(offs), i(toks), i(pars),
+                                                          i(lens))
+            rc = f.L.spec_verify_noalloc(ctypes.byref(f.c), ctypes.byref(f.w), f.kv, len(ids),
+                                         p1, p2, p3, p4, p5, None, ctypes.c_void_p(FAKE_DEV),
+                                         ctypes.c_void_p(FAKE_DEV), ctypes.c_void_p(FAKE_DEV),
+                                         None)
+            return rc, f.L.spec_last_error().decode()
+        tree = (list(range(16)), [-1] + list(range(15)))
+        assert sv.spec_workspace_bytes(cfg, 256, 4096) > B.SPEC_NOALLOC_SCRATCH_BYTES
+        rc, msg = call(list(range(256)), [tree] * 256, [100] * 256)
+        assert rc == -5 and "static scratch" in msg, msg
+        rc, msg = call([0, 1], [tree, ([1, 2], [0, 0])], [10, 10])
+        assert rc == -2, msg
+    finally:
+        f.close()
