@@ -176,9 +176,16 @@ __global__ __launch_bounds__(NW * 64, (gemm_occupancy<BM, BN, NS, BK>())) void g
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ntm = (a.M + BM - 1) / BM;
   const int tiles = ntm * (a.N / BN);
+  // Work-group b runs on XCD b % 8, which receives q + 1 work-groups (x < r)
+  // or q (x >= r) for a grid of 8q + r.  Give each XCD a contiguous range of
+  // logical ids, so that the M tiles sharing a weight tile (adjacent ids)
+  // meet in one XCD's L2.
   const int total = gridDim.x;
   int bid = blockIdx.x;
-  if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
+  {
+    const int q = total >> 3, r = total & 7, x = bid & 7, j = bid >> 3;
+    bid = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+  }
   const int tile = bid % tiles, split = bid / tiles;
   const int tm = tile % ntm, tn = tile / ntm;
   const int KT = a.K / BK / a.ksplit;            // K steps of this split
