@@ -118,7 +118,7 @@ WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_to
   L.q = take(max_tokens * nq_hd * 2);
   L.o = take(max_tokens * nq_hd * 2);
   L.act = take(max_tokens * (size_t)c->ffn * 2);
-  L.part_o = take((size_t)kPartCap * 32 * c->head_dim * 4);
+  L.part_o = take((size_t)kPartCap * 32 * c->head_dim * 2);
   L.part_ml = take((size_t)kPartCap * 32 * 2 * 4);
   L.lm_val = take(max_tokens * (size_t)(c->vocab / 64) * 4);
   L.lm_idx = take(max_tokens * (size_t)(c->vocab / 64) * 4);
@@ -546,7 +546,7 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
   aa.n_wide = (int)wide4.size();
   aa.wide8 = d_wide8;
   aa.n_wide8 = (int)wide8.size();
-  aa.part_o = (float*)(ws + ly.part_o);
+  aa.part_o = (f16*)(ws + ly.part_o);
   aa.part_ml = (float*)(ws + ly.part_ml);
   aa.out = d_o;
   aa.n_heads = nq;

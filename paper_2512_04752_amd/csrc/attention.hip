@@ -254,14 +254,17 @@ __device__ __forceinline__ void pv_block(const char* v0, const bf16x8 (&pb)[2], 
 }
 
 // Write a lane's finished row: dims 32i + 8q + 4h + {0..3} sit in
-// o[i][4q..4q+3].  nsplit == 1: normalised bf16 output; otherwise the
-// unnormalised fp32 partial and (m, l) of split slot `slot`.
+// o[i][4q..4q+3].  nsplit == 1: normalised bf16 output; otherwise the split
+// slot `slot` takes the row normalised by its own sum, o / l, in fp16 (a
+// convex combination of V rows, so within the cache's range; 11-bit
+// significand against the bf16 output's 8) and its (m, l) in fp32.  A row
+// that sees no key of this split (l = 0) stores zeros.
 template <int HD>
 __device__ __forceinline__ void store_row(const AttnArgs& a, const f32x16 (&o)[HD / 32], float m_run,
                                           float l_run, int nsplit, int slot, int r, int h,
                                           size_t out_row, int head) {
+  const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
   if (nsplit == 1) {
-    const float inv = 1.f / l_run;
     bf16* dst = a.out + out_row * (size_t)a.n_heads * HD + head * HD + 4 * h;
 #pragma unroll
     for (int i = 0; i < HD / 32; ++i)
@@ -273,13 +276,16 @@ __device__ __forceinline__ void store_row(const AttnArgs& a, const f32x16 (&o)[H
         *(bf16x4*)(dst + 32 * i + 8 * q) = v;
       }
   } else {
-    float* dst = a.part_o + ((size_t)slot * 32 + r) * HD + 4 * h;
+    f16* dst = a.part_o + ((size_t)slot * 32 + r) * HD + 4 * h;
 #pragma unroll
     for (int i = 0; i < HD / 32; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *(f32x4*)(dst + 32 * i + 8 * q) =
-            f32x4{o[i][4 * q], o[i][4 * q + 1], o[i][4 * q + 2], o[i][4 * q + 3]};
+      for (int q = 0; q < 4; ++q) {
+        f16x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = (f16)(o[i][4 * q + j] * inv);
+        *(f16x4*)(dst + 32 * i + 8 * q) = v;
+      }
     if (h == 0) {
       a.part_ml[((size_t)slot * 32 + r) * 2] = m_run;
       a.part_ml[((size_t)slot * 32 + r) * 2 + 1] = l_run;
@@ -364,7 +370,7 @@ __global__ __launch_bounds__(AttnCfg<HD>::NWN * 64, 2) void tree_attention_kerne
   const bf16* vbase = kbase + (size_t)a.n_kv_heads * head_stride;
   char* ring = smem + w * C::WAVE_RING;
 
-  // Blocks of this wave: w, w+4, w+8, ... of the item's range.
+  // Blocks of this wave: w, w + NWN, w + 2 NWN, ... of the item's range.
   const int nblk = (it.key1 - it.key0 + KBLK - 1) / KBLK;
   const int mine = nblk > w ? (nblk - w + C::NWN - 1) / C::NWN : 0;
   const int mask_from = min(si.seq_len, it.key1);   // blocks ending past this need the mask
@@ -467,7 +473,7 @@ __global__ __launch_bounds__(AttnCfg<HD>::NWN * 64, 2) void tree_attention_kerne
     if (it.nsplit == 1) {
       a.out[(size_t)(si.tok0 + nd) * nq_hd + hq * HD + d] = (bf16)(O / L);
     } else {
-      a.part_o[((size_t)it.part * 32 + row) * HD + d] = O;
+      a.part_o[((size_t)it.part * 32 + row) * HD + d] = (f16)(L > 0.f ? O / L : 0.f);
       if (d == 0) {
         a.part_ml[((size_t)it.part * 32 + row) * 2] = M;
         a.part_ml[((size_t)it.part * 32 + row) * 2 + 1] = L;
@@ -604,9 +610,11 @@ __global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void tree_attention_wide_
 
 // Merge the partial states of a row tile's key ranges.  A 256-thread block
 // takes RPB query rows of one item with HD/4 lanes per row, four consecutive
-// dimensions per lane.  A row's lanes share its splits' (m, l) to form the
-// split weights, and every split's partial output is one 16-byte load per
-// lane, four splits in flight at a time, accumulated in split order.
+// dimensions per lane.  Split s holds its normalised output o_s / l_s and
+// (m_s, l_s); its weight in the merged row is l_s 2^(m_s - M) with M the
+// largest m_s.  A row's lanes share the weights, and every split's partial
+// output is one 8-byte load per lane, four splits in flight at a time,
+// accumulated in split order.
 template <int HD>
 __global__ __launch_bounds__(256) void attention_combine_kernel(AttnArgs a) {
   constexpr int LPR = HD / 4, RPB = 256 / LPR, MAXS = 64;
@@ -630,32 +638,32 @@ __global__ __launch_bounds__(256) void attention_combine_kernel(AttnArgs a) {
   for (int sp = lane; sp < ns; sp += LPR) {
     const size_t slot = (size_t)(ci.part0 + sp) * 32 + row;
     const float ms = a.part_ml[slot * 2];
-    const float f = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M);
+    const float f = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M) * a.part_ml[slot * 2 + 1];
     wgt[rr][sp] = f;
-    L += f * a.part_ml[slot * 2 + 1];
+    L += f;
   }
 #pragma unroll
   for (int m = LPR / 2; m >= 1; m >>= 1) L += __shfl_xor(L, m);
   if (lane == 0) inv_l[rr] = 1.f / L;
   __syncthreads();
   if (!live) return;
-  const float* src = a.part_o + ((size_t)ci.part0 * 32 + row) * HD + 4 * lane;
-  constexpr size_t STRIDE = (size_t)32 * HD;   // floats between consecutive splits
+  const f16* src = a.part_o + ((size_t)ci.part0 * 32 + row) * HD + 4 * lane;
+  constexpr size_t STRIDE = (size_t)32 * HD;   // elements between consecutive splits
   f32x4 O = {0.f, 0.f, 0.f, 0.f};
   int sp = 0;
   for (; sp + 4 <= ns; sp += 4) {
-    f32x4 p[4];
+    f16x4 p[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) p[u] = *(const f32x4*)(src + (sp + u) * STRIDE);
+    for (int u = 0; u < 4; ++u) p[u] = *(const f16x4*)(src + (sp + u) * STRIDE);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) O[j] += wgt[rr][sp + u] * p[u][j];
+      for (int j = 0; j < 4; ++j) O[j] += wgt[rr][sp + u] * (float)p[u][j];
   }
   for (; sp < ns; ++sp) {
-    const f32x4 p = *(const f32x4*)(src + sp * STRIDE);
+    const f16x4 p = *(const f16x4*)(src + sp * STRIDE);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) O[j] += wgt[rr][sp] * p[j];
+    for (int j = 0; j < 4; ++j) O[j] += wgt[rr][sp] * (float)p[j];
   }
   bf16x4 v;
 #pragma unroll

@@ -14,6 +14,8 @@ typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 typedef __attribute__((ext_vector_type(2))) int i32x2;
+typedef _Float16 f16;
+typedef __attribute__((ext_vector_type(4))) _Float16 f16x4;
 
 constexpr int kMaxTree = 64;
 constexpr int kWave = 64;
@@ -130,7 +132,7 @@ struct AttnArgs {
   int n_wide;
   const AttnItem* wide8;    // 256-row items (tree_attention_wide_kernel<HD, 8>)
   int n_wide8;
-  float* part_o;            // [slots][32][head_dim]
+  f16* part_o;              // [slots][32][head_dim], the split's output divided by its l
   float* part_ml;           // [slots][32][2]
   bf16* out;                // [N][n_heads*head_dim]
   int layer, n_heads, n_kv_heads, head_dim;
