@@ -253,46 +253,6 @@ __device__ __forceinline__ void pv_block(const char* v0, const bf16x8 (&pb)[2], 
                                                     0, 0, 0);
 }
 
-// Write a lane's finished row: dims 32i + 8q + 4h + {0..3} sit in
-// o[i][4q..4q+3].  nsplit == 1: normalised bf16 output; otherwise the split
-// slot `slot` takes the row normalised by its own sum, o / l, in fp16 (a
-// convex combination of V rows, so within the cache's range; 11-bit
-// significand against the bf16 output's 8) and its (m, l) in fp32.  A row
-// that sees no key of this split (l = 0) stores zeros.
-template <int HD>
-__device__ __forceinline__ void store_row(const AttnArgs& a, const f32x16 (&o)[HD / 32], float m_run,
-                                          float l_run, int nsplit, int slot, int r, int h,
-                                          size_t out_row, int head) {
-  const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-  if (nsplit == 1) {
-    bf16* dst = a.out + out_row * (size_t)a.n_heads * HD + head * HD + 4 * h;
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        bf16x4 v;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[i][4 * q + j] * inv);
-        *(bf16x4*)(dst + 32 * i + 8 * q) = v;
-      }
-  } else {
-    f16* dst = a.part_o + ((size_t)slot * 32 + r) * HD + 4 * h;
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        f16x4 v;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = (f16)(o[i][4 * q + j] * inv);
-        *(f16x4*)(dst + 32 * i + 8 * q) = v;
-      }
-    if (h == 0) {
-      a.part_ml[((size_t)slot * 32 + r) * 2] = m_run;
-      a.part_ml[((size_t)slot * 32 + r) * 2 + 1] = l_run;
-    }
-  }
-}
-
 template <int HD>
 struct AttnCfg {
   static constexpr int ROW = HD * 2;                    // bytes per K or V row
@@ -454,27 +414,38 @@ __global__ __launch_bounds__(AttnCfg<HD>::NWN * 64, 2) void tree_attention_kerne
     }
   __syncthreads();
 
-  for (int idx = tid; idx < 32 * HD; idx += C::NWN * 64) {
-    const int row = idx / HD, d = idx % HD;
+  // Each thread merges 8 consecutive dimensions of a row and writes them as
+  // one 16-byte store (bf16 output, or the fp16 partial of a split range).
+  for (int idx = tid; idx < 32 * (HD / 8); idx += C::NWN * 64) {
+    const int row = idx / (HD / 8), d0 = (idx % (HD / 8)) * 8;
     const int gr = it.row0 + row;
     const int nd = gr / G, hq = it.kvh * G + gr % G;
     if (nd >= si.ntok) continue;
     float M = -INFINITY;
 #pragma unroll
     for (int ww = 0; ww < C::NWN; ++ww) M = fmaxf(M, ml_sh[(ww * 32 + row) * 2]);
-    float O = 0.f, L = 0.f;
+    float O[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, L = 0.f;
 #pragma unroll
     for (int ww = 0; ww < C::NWN; ++ww) {
       const float mw = ml_sh[(ww * 32 + row) * 2];
       const float f = (mw == -INFINITY) ? 0.f : fast_exp2(mw - M);
-      O += f * o_sh[(ww * 32 + row) * C::O_STRIDE + d];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) O[j] += f * o_sh[(ww * 32 + row) * C::O_STRIDE + d0 + j];
       L += f * ml_sh[(ww * 32 + row) * 2 + 1];
     }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
     if (it.nsplit == 1) {
-      a.out[(size_t)(si.tok0 + nd) * nq_hd + hq * HD + d] = (bf16)(O / L);
+      bf16x8 v;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = (bf16)(O[j] * inv);
+      *(bf16x8*)(a.out + (size_t)(si.tok0 + nd) * nq_hd + hq * HD + d0) = v;
     } else {
-      a.part_o[((size_t)it.part * 32 + row) * HD + d] = (f16)(L > 0.f ? O / L : 0.f);
-      if (d == 0) {
+      typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+      f16x8 v;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = (f16)(O[j] * inv);
+      *(f16x8*)(a.part_o + ((size_t)it.part * 32 + row) * HD + d0) = v;
+      if (d0 == 0) {
         a.part_ml[((size_t)it.part * 32 + row) * 2] = M;
         a.part_ml[((size_t)it.part * 32 + row) * 2 + 1] = L;
       }
@@ -604,8 +575,50 @@ __global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void tree_attention_wide_
   }
   l_run = sum_xor32(l_run);
 
-  if (!row_ok) return;
-  store_row<HD>(a, o, m_run, l_run, it.nsplit, it.part + w * it.nsplit, r, h, si.tok0 + node, head);
+  // Finished rows go out through LDS so that every store writes 1 KB
+  // contiguous: each wave stages its 32 rows (bf16 output or fp16 partial,
+  // both 2 bytes per element) in a private region of the now idle ring,
+  // then lane l of store k writes 16 bytes of row 4k + l/16.
+  __syncthreads();            // every wave has finished reading the last stage
+  constexpr int PITCH = HD * 2 + 16;                 // bytes per staged row
+  char* stg = smem + w * 32 * PITCH;
+  const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+  const bool split = it.nsplit > 1;
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      char* dst = stg + r * PITCH + (32 * i + 8 * q + 4 * h) * 2;
+      if (split) {
+        f16x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = (f16)(o[i][4 * q + j] * inv);
+        *(f16x4*)dst = v;
+      } else {
+        bf16x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[i][4 * q + j] * inv);
+        *(bf16x4*)dst = v;
+      }
+    }
+  const int slot = it.part + w * it.nsplit;
+  if (split && h == 0 && row_ok) {
+    a.part_ml[((size_t)slot * 32 + r) * 2] = m_run;
+    a.part_ml[((size_t)slot * 32 + r) * 2 + 1] = l_run;
+  }
+  constexpr int CPR = HD / 8;                        // 16-byte chunks per row
+  constexpr int RPS = 64 / CPR;                      // rows per 1 KB store
+#pragma unroll
+  for (int k = 0; k < 32 / RPS; ++k) {
+    const int rr = k * RPS + lane / CPR, ch = lane % CPR;
+    const i32x4 v = *(const i32x4*)(stg + rr * PITCH + ch * 16);
+    const int gr = it.row0 + 32 * w + rr;
+    const int nd = gr / G;
+    if (nd >= si.ntok) continue;
+    char* g = split ? (char*)(a.part_o + ((size_t)slot * 32 + rr) * HD)
+                    : (char*)(a.out + (size_t)(si.tok0 + nd) * nq_hd + (it.kvh * G + gr % G) * HD);
+    *(i32x4*)(g + ch * 16) = v;
+  }
 }
 
 // Merge the partial states of a row tile's key ranges.  A 256-thread block
