@@ -18,7 +18,7 @@ MUTATIONS = {
                     "return torch.cat([a * c + b * s, b * c - a * s], dim=-1)"),
     "rotary frequency": ("theta ** (-2.0 * j / head_dim)", "theta ** (-1.0 * j / head_dim)"),
     "kv head of a query head": ("kv = h // group", "kv = h % n_kv_heads"),
-    "norm gain dropped": ("+ eps) * gain", "+ eps)"),
+    "norm gain dropped": ("keepdim=True) + eps) * gain", "keepdim=True) + eps)"),
     "position = S + node index": ('"pos": S + depth,', '"pos": S + torch.arange(len(tokens)),'),
     "siblings visible": ("anc[i] = anc[p]\n", "anc[i] = anc[p] | anc[i - 1]\n"),
     "score scale dropped": ("@ k_all[kv].T) / math.sqrt(d)", "@ k_all[kv].T)"),
