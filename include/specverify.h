@@ -51,7 +51,9 @@
 extern "C" {
 #endif
 
-#define SPEC_MAX_TREE 64
+#define SPEC_MAX_TREE 256
+/* 64-bit words of one node's ancestor set (spec_debug.anc). */
+#define SPEC_ANC_WORDS (SPEC_MAX_TREE / 64)
 
 typedef enum {
   SPEC_OK = 0,
@@ -100,7 +102,8 @@ typedef struct {
   int32_t* argmax;    /* [N] greedy token after each node */
   int32_t* depth;     /* [N] depth of each node (root 0) */
   int32_t* pos;       /* [N] position S_b + depth */
-  uint64_t* anc;      /* [N] ancestor set, bit t = node t of the same tree, own bit set */
+  uint64_t* anc;      /* [N][SPEC_ANC_WORDS] ancestor set: bit t % 64 of word t / 64 is node t
+                         of the same tree; own bit set, bits of nodes >= T_b clear */
 } spec_debug;
 
 /* ---- KV pool (Section 6.2: verified KV is never rewritten) -------------

@@ -15,7 +15,8 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspecverify.so")
 
-SPEC_MAX_TREE = 64
+SPEC_MAX_TREE = 256
+SPEC_ANC_WORDS = SPEC_MAX_TREE // 64   # 64-bit words of one node's ancestor set
 STATUS = {0: "SPEC_OK", -1: "SPEC_ERR_INVALID", -2: "SPEC_ERR_TREE", -3: "SPEC_ERR_CAPACITY",
           -5: "SPEC_ERR_WORKSPACE", -6: "SPEC_ERR_UNSUPPORTED", -7: "SPEC_ERR_HIP"}
 KERNEL_CLASS = {"gemm_qkv": 0, "attention": 1, "gemm_o": 2, "gemm_gate_up": 3, "gemm_down": 4,

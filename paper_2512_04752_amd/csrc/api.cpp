@@ -111,7 +111,7 @@ WsLayout ws_layout(const spec_model_config* c, int64_t max_batch, int64_t max_to
   const size_t nq_hd = (size_t)c->n_heads * c->head_dim;
   L.blob = take(L.blob_bytes);
   L.toks = take(max_tokens * sizeof(TokInfo));
-  L.anc = take(max_tokens * 8);
+  L.anc = take(max_tokens * 8 * kAncWords);
   L.rope = take(max_tokens * (size_t)(c->head_dim / 2) * 8);
   L.x = take(max_tokens * (size_t)c->hidden * 4);
   L.h = take(max_tokens * (size_t)c->hidden * 2);

@@ -119,14 +119,20 @@ __device__ __forceinline__ float sum_xor32(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Scores of keys this lane's row may not see become -inf.
-__device__ __forceinline__ void mask_block(f32x16& s, int kb, int key1, int seq_len, uint64_t anc,
+// Scores of keys this lane's row may not see become -inf: committed keys
+// (tree index tt < 0) are visible, tree key tt is visible when node tt is an
+// ancestor, keys from key1 on never are.  The 32 keys of the block span at
+// most two words of the ancestor set, picked once.
+__device__ __forceinline__ void mask_block(f32x16& s, int kb, int key1, int seq_len, const NodeSet& anc,
                                            int h) {
+  const int t0 = kb - seq_len;
+  const uint64_t lo = anc.word(t0), hi = anc.word(t0 + 31);
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const int key = kb + 8 * (e >> 2) + 4 * h + (e & 3);
     const int tt = key - seq_len;
-    const bool anc_bit = (anc >> (tt & 63)) & 1ull;
+    const uint64_t w = (tt >> 6) == (t0 >> 6) ? lo : hi;
+    const bool anc_bit = (w >> (tt & 63)) & 1ull;
     const bool vis = (key < key1) & ((tt < 0) | anc_bit);
     s[e] = vis ? s[e] : -INFINITY;
   }
@@ -137,7 +143,7 @@ __device__ __forceinline__ void mask_block(f32x16& s, int kb, int key1, int seq_
 // of the output for both.
 template <int NB>
 __device__ __forceinline__ void softmax_stage(bool mask_a, bool mask_b, f32x16& sa, f32x16& sb, int kb,
-                                              int key1, int seq_len, uint64_t anc, int h, float sl2,
+                                              int key1, int seq_len, const NodeSet& anc, int h, float sl2,
                                               float& m_run, float& l_run, f32x16 (&o)[NB],
                                               bf16x8 (&pa)[2], bf16x8 (&pb)[2]) {
   if (mask_a) mask_block(sa, kb, key1, seq_len, anc, h);
@@ -200,19 +206,10 @@ __device__ __forceinline__ bf16x8 vt_fragment(const char* v0, int kst, int i, in
 // maximum of the scaled scores (base-2 domain).  Produces P^T in bf16 and
 // accumulates the row sum of the unrounded probabilities.
 template <bool MASK, int NB>
-__device__ __forceinline__ void softmax_block(f32x16& s, int kb, int key1, int seq_len, uint64_t anc,
+__device__ __forceinline__ void softmax_block(f32x16& s, int kb, int key1, int seq_len, const NodeSet& anc,
                                               int h, float sl2, float& m_run, float& l_run,
                                               f32x16 (&o)[NB], bf16x8 (&pb)[2]) {
-  if constexpr (MASK) {
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = kb + 8 * (e >> 2) + 4 * h + (e & 3);
-      const int tt = key - seq_len;
-      const bool anc_bit = (anc >> (tt & 63)) & 1ull;
-      const bool vis = (key < key1) & ((tt < 0) | anc_bit);
-      s[e] = vis ? s[e] : -INFINITY;
-    }
-  }
+  if constexpr (MASK) mask_block(s, kb, key1, seq_len, anc, h);
   float smax = s[0];
 #pragma unroll
   for (int e = 1; e < 16; ++e) smax = fmaxf(smax, s[e]);
@@ -240,7 +237,7 @@ __device__ __forceinline__ void softmax_block(f32x16& s, int kb, int key1, int s
 
 template <int NB>
 __device__ __forceinline__ void softmax_any(bool mask, f32x16& s, int kb, int key1, int seq_len,
-                                            uint64_t anc, int h, float sl2, float& m_run,
+                                            const NodeSet& anc, int h, float sl2, float& m_run,
                                             float& l_run, f32x16 (&o)[NB], bf16x8 (&pb)[2]) {
   if (mask) softmax_block<true, NB>(s, kb, key1, seq_len, anc, h, sl2, m_run, l_run, o, pb);
   else softmax_block<false, NB>(s, kb, key1, seq_len, anc, h, sl2, m_run, l_run, o, pb);
@@ -328,7 +325,10 @@ __global__ __launch_bounds__(AttnCfg<HD>::NWN * 64, 2) void tree_attention_kerne
     qf[ks] = *(const bf16x8*)(qrow + ks * 16 + h * 8);
     if (!row_ok) qf[ks] = bf16x8{};
   }
-  const uint64_t anc_row = row_ok ? a.anc[si.tok0 + node] : 1ull;
+  // At most 32 rows per KV head: the tree has at most 32 nodes, all in word 0.
+  NodeSet anc_row;
+  anc_row.clear();
+  anc_row.w0 = row_ok ? a.anc[(size_t)(si.tok0 + node) * kAncWords] : 1ull;
 
   const size_t head_stride = (size_t)si.cap * HD;
   const bf16* kbase = a.kv_pool + si.kv_base + ((size_t)a.layer * 2 * a.n_kv_heads + it.kvh) * head_stride;
@@ -497,7 +497,10 @@ __global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void tree_attention_wide_
     qf[ks] = *(const bf16x8*)(qrow + ks * 16 + h * 8);
     if (!row_ok) qf[ks] = bf16x8{};
   }
-  const uint64_t anc_row = row_ok ? a.anc[si.tok0 + node] : 1ull;
+  NodeSet anc_row;
+  anc_row.clear();
+  anc_row.w0 = 1ull;
+  if (row_ok) anc_row.load(a.anc + (size_t)(si.tok0 + node) * kAncWords);
 
   const size_t head_stride = (size_t)si.cap * HD;
   const bf16* kbase = a.kv_pool + si.kv_base + ((size_t)a.layer * 2 * a.n_kv_heads + it.kvh) * head_stride;

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "specverify.h"
+
 namespace spec {
 
 typedef __bf16 bf16;
@@ -17,7 +19,32 @@ typedef __attribute__((ext_vector_type(2))) int i32x2;
 typedef _Float16 f16;
 typedef __attribute__((ext_vector_type(4))) _Float16 f16x4;
 
-constexpr int kMaxTree = 64;
+constexpr int kMaxTree = SPEC_MAX_TREE;        // nodes per draft tree
+constexpr int kAncWords = kMaxTree / 64;       // 64-bit words of a node's ancestor set
+static_assert(kMaxTree % 64 == 0 && kAncWords == SPEC_ANC_WORDS, "ancestor words");
+
+// A set of nodes of one tree held in registers: bit t % 64 of word t / 64.
+// Four named words, picked by compare-and-select, so that the set never
+// needs dynamic register indexing (which would put it in scratch memory).
+struct NodeSet {
+  uint64_t w0, w1, w2, w3;
+  __device__ __forceinline__ void clear() { w0 = w1 = w2 = w3 = 0ull; }
+  __device__ __forceinline__ void load(const uint64_t* p) { w0 = p[0]; w1 = p[1]; w2 = p[2]; w3 = p[3]; }
+  __device__ __forceinline__ uint64_t word(int t) const {
+    const int k = t >> 6;
+    return k == 0 ? w0 : k == 1 ? w1 : k == 2 ? w2 : w3;
+  }
+  __device__ __forceinline__ bool has(int t) const { return (word(t) >> (t & 63)) & 1ull; }
+  __device__ __forceinline__ void add(int t) {
+    const int k = t >> 6;
+    const uint64_t bit = 1ull << (t & 63);
+    w0 |= k == 0 ? bit : 0ull;
+    w1 |= k == 1 ? bit : 0ull;
+    w2 |= k == 2 ? bit : 0ull;
+    w3 |= k == 3 ? bit : 0ull;
+  }
+};
+static_assert(kAncWords == 4, "NodeSet holds four words");
 constexpr int kWave = 64;
 
 // Per live sample, built on the host for every verify call.
@@ -125,7 +152,7 @@ struct AttnArgs {
   const bf16* kv_pool;
   const SampleInfo* samples;
   const TokInfo* toks;
-  const uint64_t* anc;      // [N]
+  const uint64_t* anc;      // [N][kAncWords] ancestor sets (NodeSet words)
   const AttnItem* items;    // 32-row items (tree_attention_kernel)
   int n_items;
   const AttnItem* wide;     // 128-row items (tree_attention_wide_kernel<HD, 4>)

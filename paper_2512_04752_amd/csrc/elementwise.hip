@@ -9,34 +9,50 @@ namespace spec {
 
 namespace {
 
-// Depth, position and ancestor set of every node: one wave per sample, lane
-// i = node i (a tree has at most 64 nodes).  Pointer jumping: lane i holds
-// the set of its ancestors at distance < 2^r and its ancestor at distance
-// 2^r (the root points at itself); six rounds of "set |= set of that
-// ancestor, jump to its jump" cover every depth up to 63.  Depth is the set's
-// size minus one.
-__global__ __launch_bounds__(256) void tree_meta_kernel(const SampleInfo* samples, int batch,
-                                                        const int32_t* parents, TokInfo* toks,
-                                                        uint64_t* anc, int32_t* dbg_depth,
-                                                        int32_t* dbg_pos, uint64_t* dbg_anc) {
-  const int b = blockIdx.x * 4 + (threadIdx.x >> 6), i = threadIdx.x & 63;
-  if (b >= batch) return;
+// Depth, position and ancestor set of every node: one work-group per sample,
+// thread i = node i (a tree has at most kMaxTree nodes).  The set is
+// kAncWords 64-bit words, bit t % 64 of word t / 64 standing for node t.
+// Pointer jumping: node i holds the set of its ancestors at distance < 2^r
+// and its ancestor at distance 2^r (the root points at itself); each round
+// publishes both in LDS and takes "set |= set of that ancestor, jump to its
+// jump", so ceil(log2 T) rounds cover every depth below T.  Depth is the
+// set's size minus one.
+__global__ __launch_bounds__(kMaxTree) void tree_meta_kernel(const SampleInfo* samples,
+                                                             const int32_t* parents, TokInfo* toks,
+                                                             uint64_t* anc, int32_t* dbg_depth,
+                                                             int32_t* dbg_pos, uint64_t* dbg_anc) {
+  __shared__ uint64_t sset[kMaxTree][kAncWords];
+  __shared__ int sjump[kMaxTree];
+  const int b = blockIdx.x, i = threadIdx.x;
   const SampleInfo s = samples[b];
   const bool live = i < s.ntok;
   int jump = (live && i > 0) ? parents[s.tok0 + i] : i;
-  uint64_t set = 1ull << i;
+  uint64_t set[kAncWords];
 #pragma unroll
-  for (int r = 0; r < 6; ++r) {
-    set |= __shfl(set, jump);
-    jump = __shfl(jump, jump);
+  for (int w = 0; w < kAncWords; ++w) set[w] = w == (i >> 6) ? 1ull << (i & 63) : 0ull;
+  for (int r = 0; (1 << r) < s.ntok; ++r) {     // same bound in every thread of the sample
+#pragma unroll
+    for (int w = 0; w < kAncWords; ++w) sset[i][w] = set[w];
+    sjump[i] = jump;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kAncWords; ++w) set[w] |= sset[jump][w];
+    jump = sjump[jump];
+    __syncthreads();
   }
   if (!live) return;
-  const int row = s.tok0 + i, depth = __popcll(set) - 1;
+  int size = 0;
+#pragma unroll
+  for (int w = 0; w < kAncWords; ++w) size += __popcll(set[w]);
+  const int row = s.tok0 + i, depth = size - 1;
   toks[row] = TokInfo{b, i, s.seq_len + depth, depth};
-  anc[row] = set;
+#pragma unroll
+  for (int w = 0; w < kAncWords; ++w) {
+    anc[(size_t)row * kAncWords + w] = set[w];
+    if (dbg_anc) dbg_anc[(size_t)row * kAncWords + w] = set[w];
+  }
   if (dbg_depth) dbg_depth[row] = depth;
   if (dbg_pos) dbg_pos[row] = s.seq_len + depth;
-  if (dbg_anc) dbg_anc[row] = set;
 }
 
 // cos/sin of position * theta^(-2j/d), angles in double precision.
@@ -133,13 +149,15 @@ __global__ void accept_kernel(const SampleInfo* samples, int batch, const int32_
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= batch) return;
   const SampleInfo s = samples[b];
-  uint64_t acc = 1ull;
+  NodeSet acc;
+  acc.clear();
+  acc.add(0);
   int best = 0, best_depth = 0;
   for (int i = 1; i < s.ntok; ++i) {
     const int row = s.tok0 + i;
     const int p = parents[row];
-    if (((acc >> p) & 1ull) && tokens[row] == argmax[s.tok0 + p]) {
-      acc |= 1ull << i;
+    if (acc.has(p) && tokens[row] == argmax[s.tok0 + p]) {
+      acc.add(i);
       const int d = toks[row].depth;
       if (d > best_depth) { best_depth = d; best = i; }
     }
@@ -211,8 +229,8 @@ __global__ __launch_bounds__(256) void compact_kernel(const SampleInfo* samples,
 hipError_t launch_tree_meta(const SampleInfo* samples, int batch, const int32_t* parents,
                             TokInfo* toks, uint64_t* anc, int32_t* dbg_depth, int32_t* dbg_pos,
                             uint64_t* dbg_anc, hipStream_t s) {
-  tree_meta_kernel<<<(batch + 3) / 4, 256, 0, s>>>(samples, batch, parents, toks, anc, dbg_depth,
-                                                    dbg_pos, dbg_anc);
+  tree_meta_kernel<<<batch, kMaxTree, 0, s>>>(samples, parents, toks, anc, dbg_depth, dbg_pos,
+                                               dbg_anc);
   return hipGetLastError();
 }
 

@@ -697,13 +697,15 @@ __global__ void accept_eos_kernel(const SampleInfo* samples, int batch, const in
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= batch) return;
   const SampleInfo s = samples[b];
-  uint64_t open = tokens[s.tok0] == eos ? 0ull : 1ull;   // accepted and not EOS: may have children
+  NodeSet open;                                   // accepted and not EOS: may have children
+  open.clear();
+  if (tokens[s.tok0] != eos) open.add(0);
   int best = 0, best_depth = 0;
   for (int i = 1; i < s.ntok; ++i) {
     const int row = s.tok0 + i;
     const int p = parents[row];
-    if (((open >> p) & 1ull) && tokens[row] == argmax[s.tok0 + p]) {
-      if (tokens[row] != eos) open |= 1ull << i;
+    if (open.has(p) && tokens[row] == argmax[s.tok0 + p]) {
+      if (tokens[row] != eos) open.add(i);
       const int d = toks[row].depth;
       if (d > best_depth) { best_depth = d; best = i; }
     }

@@ -43,7 +43,7 @@ class Verifier:
         d = {"argmax": torch.empty(n_tokens, dtype=torch.int32, device=dev),
              "depth": torch.empty(n_tokens, dtype=torch.int32, device=dev),
              "pos": torch.empty(n_tokens, dtype=torch.int32, device=dev),
-             "anc": torch.empty(n_tokens, dtype=torch.int64, device=dev)}
+             "anc": torch.empty(n_tokens, B.SPEC_ANC_WORDS, dtype=torch.int64, device=dev)}
         if logits:
             d["logits"] = torch.empty(n_tokens, self.cfg.vocab, dtype=torch.float32, device=dev)
         return d

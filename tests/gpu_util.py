@@ -193,7 +193,9 @@ def check_meta(trees, lens, out):
         assert out["depth"][sl].tolist() == depth.tolist()
         assert out["pos"][sl].tolist() == (int(lens[b]) + depth).tolist()
         bits = [sum(1 << j for j in range(len(parents)) if anc[i, j]) for i in range(len(parents))]
-        got = [int(x) & ((1 << 64) - 1) for x in out["anc"][sl].tolist()]
+        # word w of a node holds nodes 64w .. 64w + 63
+        got = [sum((int(x) & ((1 << 64) - 1)) << (64 * w) for w, x in enumerate(words))
+               for words in out["anc"][sl].tolist()]
         assert got == bits
 
 

@@ -148,7 +148,8 @@ def test_validation_errors(fake, case, code):
     elif case == "empty_tree":
         trees = [GOOD, ([], [])]
     elif case == "too_big_tree":
-        trees = [GOOD, ([1] * 65, wl.chain_tree(65))]
+        n = B.SPEC_MAX_TREE + 1
+        trees = [GOOD, ([1] * n, wl.chain_tree(n))]
     elif case == "capacity":
         lens = [10, 198]
     elif case == "dup_sample":

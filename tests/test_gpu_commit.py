@@ -1,6 +1,6 @@
 """GPU parity of KV compaction (spec_kv_commit) against the oracle's commit,
 through the C ABI, on accepted branches deeper and wider than the verify tests
-reach: whole 64-node chains, branches that jump over most of the tree, and
+reach: whole chains of the largest tree, branches that jump over most of the tree, and
 batches large enough that one work-group moves every K/V head of a layer in
 several passes.  Pools hold random bit patterns, so a misplaced element cannot
 match by accident; the comparison is bitwise."""
@@ -19,7 +19,7 @@ from tests.test_gpu_transfer import random_pool, views
 
 pytestmark = pytest.mark.gpu
 
-MAX_TREE = 64
+MAX_TREE = sv.SPEC_MAX_TREE
 
 
 def random_branch(rng, depth):
@@ -39,7 +39,7 @@ def random_branch(rng, depth):
 
 CASES = {
     # (config, batch, seed).  At the 8B shape batch 40 puts all 16 K/V heads of
-    # a layer in one work-group (64-deep branches take 8 passes) and batch 4
+    # a layer in one work-group (a branch as deep as the largest tree takes many passes) and batch 4
     # two heads; the 2-layer and tiny cases give one head per work-group.
     "llama8b_b40": (wl.LLAMA_8B, 40, 0),
     "llama8b_b4": (wl.LLAMA_8B, 4, 1),

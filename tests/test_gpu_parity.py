@@ -119,6 +119,54 @@ def test_tiny_edge_cases():
     full_check(cfg, W_cpu, ver, ids, trees, lens)
 
 
+def test_tiny_large_trees_and_commit():
+    """Trees past one 64-bit ancestor word (65 to 256 nodes): multi-word
+    ancestor sets in the metadata, the 8-wave attention over two 256-row
+    groups, an accepted branch deeper than 64 (a chain steered along the
+    oracle's greedy choice for 80 levels) and its commit."""
+    cfg = wl.TINY
+    say("tiny large trees: 256, 200 (chain), 130, 65 (star), 129 nodes")
+    W_cpu = wl.make_weights(cfg, 34, dtype=torch.bfloat16)
+    W_dev = {"tok_embed": W_cpu["tok_embed"].cuda(), "final_norm": W_cpu["final_norm"].cuda(),
+             "lm_head": W_cpu["lm_head"].cuda(),
+             "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
+    rng = np.random.default_rng(21)
+    pars = [wl.recursive_tree(rng, 256, 10, 4), wl.chain_tree(200), wl.recursive_tree(rng, 130, 12, 3),
+            [-1] + [0] * 64, wl.recursive_tree(rng, 129, 9, 4)]
+    assert max(len(p) for p in pars) == sv.SPEC_MAX_TREE
+    lens = [100, 37, 0, 180, 64]
+    caps = [S + len(p) + 8 for S, p in zip(lens, pars)]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=5, max_tokens=sum(len(p) for p in pars))
+    gen = torch.Generator(device="cuda").manual_seed(21)
+    ids = list(range(5))
+    for i, S in zip(ids, lens):
+        k, v = ver.kv.sample_view(i)
+        wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    trees = [(wl.random_tokens(rng, len(p), cfg.vocab), p) for p in pars]
+    branches = [wl.deepest_branch(p, rng) for p in pars]
+    branches[1] = branches[1][:80]          # the chain: 79 levels past the root
+    wl.follow_greedy(trees, branches, 1.0, oracle_greedy_fn(cfg, W_cpu, ver, ids, lens), rng)
+    out, r, exc = full_check(cfg, W_cpu, ver, ids, trees, lens)
+    check_tree_kv(cfg, ver, ids, trees, lens, r, ids)
+    acc = out["accepted_len"]
+    say(f"  accepted {acc}")
+    assert acc[1] > 64, "the steered chain is accepted past the first ancestor word"
+    pre = [pool_bytes(ver, b, 0, lens[b] + len(pars[b])) for b in ids]
+    new_lens = ver.commit(ids, lens)
+    torch.cuda.synchronize()
+    new_lens = new_lens.cpu().tolist()
+    for b in ids:
+        path = out["nodes"][b][:acc[b] + 1].tolist()
+        assert new_lens[b] == lens[b] + acc[b] + 1
+        k, v = pool_bytes(ver, b, 0, lens[b] + acc[b] + 1)
+        S = lens[b]
+        for d, node in enumerate(path):
+            assert torch.equal(k[:, :, S + d], pre[b][0][:, :, S + node])
+            assert torch.equal(v[:, :, S + d], pre[b][1][:, :, S + node])
+    release(ver, W_dev)
+
+
 def test_tiny_repeat_is_bitwise_identical():
     say("tiny repeatability")
     cfg, w, W_cpu, W_dev, ver = tiny_setup(5)
@@ -216,6 +264,25 @@ def test_two_layer_few_rows(batch, budget):
     W_dev = wl.make_weights(w.cfg, 60 + budget, device="cuda")
     W_cpu = cpu_weights(W_dev)
     ver = device_setup(w, W_dev, seed=7)
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    check = sorted({0, w.batch - 1})
+    out, r, exc = full_check(w.cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check,
+                             envelope=True)
+    check_tree_kv(w.cfg, ver, ids, w.trees, lens, r, check, layers=1)
+    release(ver, W_dev)
+
+
+@pytest.mark.parametrize("batch,budget", [(2, 256), (4, 96)])
+def test_two_layer_large_trees(batch, budget):
+    """8B shapes with trees past one ancestor word: top-n draft-logit trees
+    of 96 and 256 nodes (384 and 1024 query rows per KV head, i.e. two and
+    four 256-row groups of the 8-wave attention, each with its own words of
+    the ancestor sets)."""
+    w = shallow(wl.sweep_workload(batch, budget))
+    say(f"{w.name}: 2-layer 8B-shape model, {w.n_tokens} nodes")
+    W_dev = wl.make_weights(w.cfg, 80 + budget, device="cuda")
+    W_cpu = cpu_weights(W_dev)
+    ver = device_setup(w, W_dev, seed=8)
     ids, lens = list(range(w.batch)), w.seq_lens.tolist()
     check = sorted({0, w.batch - 1})
     out, r, exc = full_check(w.cfg, W_cpu, ver, ids, w.trees, lens, check_ids=check,

@@ -71,7 +71,7 @@ def test_selection_validation(case):
     elif case == "negative":
         w = [1.0, -0.1, 0.2]
     elif case == "n_max":
-        n_max = 65
+        n_max = sv.SPEC_MAX_TREE + 1
     elif case == "empty":
         offs, pars, w = [0, 0], [], []
     with pytest.raises(sv.SpecError):
