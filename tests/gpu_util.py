@@ -300,7 +300,7 @@ def shallow(w, layers=2):
     return w
 
 
-def tiny_setup(seed=0, batch=4, chain=4, extra_cap=64, sampling=False):
+def tiny_setup(seed=0, batch=4, chain=4, extra_cap=64, sampling=False, max_tokens=None):
     """The 2-layer workload: bf16-rounded weights, oracle prefill of each
     128-token prompt written into the pool, root = the oracle's greedy token
     after the prompt, chain drafts following the oracle's greedy choice."""
@@ -311,7 +311,8 @@ def tiny_setup(seed=0, batch=4, chain=4, extra_cap=64, sampling=False):
              "lm_head": W_cpu["lm_head"].cuda(),
              "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
     caps = [int(s) + extra_cap for s in w.seq_lens]
-    ver = sv.Verifier(cfg, W_dev, caps, max_batch=batch, max_tokens=batch * 64, sampling=sampling)
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=batch, max_tokens=max_tokens or batch * 64,
+                      sampling=sampling)
     for b, prompt in enumerate(w.prompts):
         pk, pv, logits = oracle.prefill(cfg, W_cpu, prompt, cache_dtype=torch.bfloat16)
         k, v = ver.kv.sample_view(b)

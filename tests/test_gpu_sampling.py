@@ -160,6 +160,33 @@ def test_tiny_sampled_matches_oracle(T):
     release(ver, W_dev)
 
 
+def test_tiny_sampled_large_trees():
+    """T = 1 over trees past one 64-bit ancestor word: random trees of 256,
+    130 and 65 nodes and a root with 199 children (far more rejected
+    children than the recomputed residuals cover, so the walk continues on
+    the stored residual row)."""
+    cfg, w, W_cpu, W_dev, ver = tiny_setup(seed=8, batch=4, extra_cap=256, sampling=True,
+                                           max_tokens=4 * 256)
+    rng = np.random.default_rng(98)
+    pars = [random_parents(rng, 256), random_parents(rng, 130), [-1] + [0] * 199,
+            random_parents(rng, 65)]
+    trees = [([w.trees[b][0][0]] + [0] * (len(p) - 1), p) for b, p in enumerate(pars)]
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    q_all = fill_tokens_by_level(ver, ids, trees, lens, 1.0, mix=0.6, seed=99)
+    N = sum(len(t[0]) for t in trees)
+    U = uniforms_for(N, 100)
+    dbg = ver.debug_buffers(N, logits=True)
+    acc, nxt, nodes = ver.verify_sampled(ids, trees, lens, 1.0, -1, q_all,
+                                         torch.from_numpy(U).cuda(), debug=dbg)
+    torch.cuda.synchronize()
+    out = {"logits": dbg["logits"].cpu(), "accepted_len": acc.cpu().tolist(),
+           "next_token": nxt.cpu().tolist(), "nodes": nodes.cpu()}
+    exact, excused, accepted, rejected = check_sampled(trees, out, q_all, U, 1.0, -1)
+    say(f"  exact {exact}, excused {excused}, accepted lengths {out['accepted_len']}")
+    assert exact + excused == len(trees) and exact >= 3
+    release(ver, W_dev)
+
+
 def rejections(pars, path):
     """Children rejected at each node of an accepted path (the oracle's walk):
     those before the taken child, all of them at the last node."""
@@ -251,6 +278,46 @@ def greedy_chains(ver, ids, trees, lens, p_follow, rng):
         for b, (toks, pars) in enumerate(trees):
             if d < len(toks) and rng.random() < p_follow:
                 toks[d] = g[offs[b] + pars[d]]
+
+
+def test_tiny_greedy_with_eos_large_trees():
+    """Greedy acceptance with EOS on chains of up to 256 nodes that follow the
+    GPU's greedy choice: one accepted to its end (past depth 64), one cut
+    where its greedy token equals the EOS token, one by a wrong token at node
+    90; the oracle's rule on the GPU's own argmax, bitwise."""
+    cfg, w, W_cpu, W_dev, ver = tiny_setup(seed=9, batch=3, extra_cap=256, sampling=True,
+                                           max_tokens=3 * 256)
+    rng = np.random.default_rng(91)
+    sizes = [120, 200, 256]
+    trees = [([w.trees[b][0][0]] + [0] * (n - 1), list(range(-1, n - 1))) for b, n in enumerate(sizes)]
+    ids, lens = list(range(w.batch)), w.seq_lens.tolist()
+    greedy_chains(ver, ids, trees, lens, 1.0, rng)
+    # EOS: chain 1's greedy token at the first node from 100 on that chain 0 never
+    # carries (greedy chains of a small model can cycle), so chain 0 runs to its end;
+    # failing that, a token no chain carries
+    seen0 = set(trees[0][0])
+    pick = [i for i in range(100, 200) if trees[1][0][i] not in seen0]
+    if pick:
+        eos = int(trees[1][0][pick[0]])
+    else:
+        eos = min(set(range(cfg.vocab)) - set().union(*(set(t[0]) for t in trees)))
+    trees[2][0][90] = (trees[2][0][90] + 1) % cfg.vocab
+    offs = split_rows(trees)
+    dbg = ver.debug_buffers(offs[-1], logits=False)
+    acc, nxt, nodes = ver.verify_sampled(ids, trees, lens, 0.0, eos, None, None, debug=dbg)
+    torch.cuda.synchronize()
+    g = dbg["argmax"].cpu().tolist()
+    lens_got = []
+    for b, (toks, pars) in enumerate(trees):
+        want = SA.greedy_accept_eos(toks, pars, g[offs[b]:offs[b + 1]], eos)
+        got_len = int(acc[b])
+        got = (got_len, int(nxt[b]), nodes[b, :got_len + 1].cpu().tolist())
+        assert got == want, f"sample {b}: gpu {got[:2]} oracle {want[:2]}"
+        assert (nodes[b, got_len + 1:] == -1).all()
+        lens_got.append(got_len)
+    say(f"  accepted lengths {lens_got}")
+    assert max(lens_got) > 64
+    release(ver, W_dev)
 
 
 def test_tiny_greedy_with_eos_is_bit_exact():
