@@ -440,6 +440,157 @@ __global__ __launch_bounds__(NW * 64, (gemm_occupancy<BM, BN, NS, BK>())) void g
   }
 }
 
+// ---- few rows: the product is a stream of the weight rows -----------------
+//
+// One work-group of 4 waves owns one unit of 16 weight rows and splits K into
+// four quarters, one per wave.  A wave multiplies with
+// v_mfma_f32_16x16x32_bf16: A = the activation rows (zero from row M on),
+// B = its 16 weight rows; lane l loads 16 bytes of row l % 16 at k-offset
+// 8 (l / 16), so a wave reads 512 contiguous bytes of each row per 256-wide
+// step, and the next step's loads are in flight while the current one is
+// multiplied.  The quarters' 16 x 16 tiles meet in LDS and wave 0 sums them
+// in wave order (a fixed order: bitwise reproducible) and applies the
+// epilogue; no K split leaves the work-group, so no reduction kernel follows
+// (a residual product leaves its RMSNorm to the caller).  Units: QKV = 8
+// rotary pairs (dims j, j + d/2) of one head, GATE_UP = 8 (gate, up)
+// features, RESID = 16 output columns.  Every unit reads all M activation
+// rows, so the activation bytes grow with M against a fixed weight stream;
+// past skinny_max_rows() the tile kernel's 256-row weight tiles win, and the
+// LM head always takes the tile kernel.  Accumulator layout of the 16 x 16
+// block: lane l, element i holds activation row 4 (l / 16) + i and unit row
+// l % 16.
+constexpr int kSkinnyRows = 16;
+// Rows up to which a product takes this path (measured on the 8B shape
+// against the tile kernel with its K splits): q/k/v and gate/up up to 4 rows
+// (at 8 rows the activation re-reads already cost more than the saved
+// reductions); the residual products up to 8 (at 16 rows the RMSNorm that
+// then runs on its own costs more than the fused split-K reduction it
+// replaces).
+template <int EPI>
+constexpr int skinny_max_rows() { return EPI == EPI_RESID ? 8 : 4; }
+
+template <int EPI>
+__device__ __forceinline__ const bf16* skinny_row(const GemmArgs& a, int unit, int c) {
+  if constexpr (EPI == EPI_QKV) {
+    const int hd = a.head_dim, upd = hd / 16;       // units per head
+    const int head_all = unit / upd, jb = unit % upd;
+    const int nh0 = a.n0 / hd, nh1 = a.n1 / hd;
+    const bf16* base;
+    int head;
+    if (head_all < nh0) { base = a.B0; head = head_all; }
+    else if (head_all < nh0 + nh1) { base = a.B1; head = head_all - nh0; }
+    else { base = a.B2; head = head_all - nh0 - nh1; }
+    const int dim = c < 8 ? jb * 8 + c : hd / 2 + jb * 8 + (c - 8);
+    return base + (size_t)(head * hd + dim) * a.K;
+  } else if constexpr (EPI == EPI_GATE_UP) {
+    const int f = unit * 8 + (c & 7);
+    return (c < 8 ? a.B0 : a.B1) + (size_t)f * a.K;
+  } else {
+    return a.B0 + (size_t)(unit * kSkinnyRows + c) * a.K;
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void skinny_gemm_kernel(GemmArgs a) {
+  static_assert(EPI != EPI_ARGMAX, "the LM head streams its rows through the tile kernel");
+  __shared__ f32x4 red[4][64];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c = lane & 15, kq = lane >> 4;
+  const int unit = blockIdx.x;
+  const int kw = a.K / 4;                            // K of this wave (a multiple of 32)
+  const int k0 = wave * kw, k1 = k0 + kw;
+  const bf16* wrow = skinny_row<EPI>(a, unit, c) + kq * 8;
+  const bool arow_ok = c < a.M;
+  const bf16* arow = a.A + (size_t)(arow_ok ? c : 0) * a.K + kq * 8;
+
+  constexpr int KB = 8;                              // 32-wide k-blocks per step
+  bf16x8 bw[2][KB], ba[2][KB];
+  auto load = [&](int set, int k) {
+#pragma unroll
+    for (int j = 0; j < KB; ++j) {
+      const int kk = k + j * 32;
+      const bool in = kk < k1;
+      bw[set][j] = in ? *(const bf16x8*)(wrow + kk) : bf16x8{};
+      ba[set][j] = in && arow_ok ? *(const bf16x8*)(arow + kk) : bf16x8{};
+    }
+  };
+  f32x4 acc = f32x4{};
+  auto mfmas = [&](int set) {
+#pragma unroll
+    for (int j = 0; j < KB; ++j) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ba[set][j], bw[set][j], acc, 0, 0, 0);
+  };
+  load(0, k0);
+  for (int k = k0; k < k1; k += 2 * KB * 32) {
+    if (k + KB * 32 < k1) load(1, k + KB * 32);
+    mfmas(0);
+    if (k + KB * 32 >= k1) break;
+    if (k + 2 * KB * 32 < k1) load(0, k + 2 * KB * 32);
+    mfmas(1);
+  }
+
+  const int m0 = 4 * kq;                             // first activation row of this lane's elements
+  {
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (wave != 0) return;
+    f32x4 t = red[0][lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) t += red[w][lane];
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + i;
+        if (m < a.M) a.x[(size_t)m * a.N + unit * kSkinnyRows + c] += t[i];
+      }
+    } else if constexpr (EPI == EPI_GATE_UP) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float u = __shfl_xor(t[i], 8);         // lanes c and c + 8: gate and up of one feature
+        const int m = m0 + i;
+        if (c < 8 && m < a.M) a.act_out[(size_t)m * (a.N / 2) + unit * 8 + c] = (bf16)(silu(t[i]) * u);
+      }
+    } else {  // EPI_QKV: lanes c < 8 hold dims j, lanes c + 8 their partners j + d/2
+      const int hd = a.head_dim, half = hd / 2, upd = hd / 16;
+      const int head_all = unit / upd, jb = unit % upd;
+      const int nh0 = a.n0 / hd, nh1 = a.n1 / hd;
+      const int seg = head_all < nh0 ? 0 : (head_all < nh0 + nh1 ? 1 : 2);
+      const int head = head_all - (seg == 0 ? 0 : (seg == 1 ? nh0 : nh0 + nh1));
+      const int j = jb * 8 + (c & 7);               // rotary frequency index of the pair
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float other = __shfl_xor(t[i], 8);
+        const int m = m0 + i;
+        if (m >= a.M) continue;
+        const float x1 = c < 8 ? t[i] : other, x2 = c < 8 ? other : t[i];
+        float y = t[i];
+        if (seg < 2) {
+          const float2 cs = a.rope_cs[(size_t)m * half + j];
+          y = c < 8 ? x1 * cs.x - x2 * cs.y : x2 * cs.x + x1 * cs.y;
+        }
+        const int dim = c < 8 ? j : j + half;
+        if (seg == 0) {
+          a.q_out[(size_t)m * a.n0 + head * hd + dim] = (bf16)y;
+        } else {
+          const TokInfo tk = a.toks[m];
+          const SampleInfo sv = a.samples[tk.sample];
+          a.kv_pool[sv.kv_base + ((((size_t)a.layer * 2 + (seg - 1)) * a.n_kv_heads + head) * sv.cap +
+                                  sv.seq_len + tk.node) * hd + dim] = (bf16)y;
+        }
+      }
+    }
+  }
+}
+
+template <int EPI>
+hipError_t launch_skinny(const GemmArgs& a, hipStream_t s) {
+  long grid;
+  if constexpr (EPI == EPI_QKV) grid = (long)(a.n0 + a.n1 + a.n2) / kSkinnyRows;
+  else grid = (long)a.N / kSkinnyRows;
+  if (a.norm_done) *a.norm_done = false;
+  skinny_gemm_kernel<EPI><<<(unsigned)grid, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 // Sum the K splits in split order and apply the epilogue.  Thread (row,
 // group g of 64 virtual columns, lane column c) owns virtual columns g*64 + c
 // and g*64 + 32 + c: pair (g % (BN/64)) of tile g / (BN/64), or two residual
@@ -613,6 +764,10 @@ hipError_t launch_tile(GemmArgs a, hipStream_t s) {
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+  // Few rows: every supported shape has K a multiple of 128 and head_dim 64
+  // or 128, which the weight-row units assume.
+  if constexpr (EPI != EPI_ARGMAX)
+    if (a.M <= skinny_max_rows<EPI>() && a.K % 128 == 0) return launch_skinny<EPI>(a, s);
   switch (pick_tile(EPI, a.M, a.N, a.K, a.n0, a.n1)) {
     case TILE_256x256: return launch_tile<EPI, 256, 256, 2, 4, 32, 8>(a, s);
     case TILE_256x128: return launch_tile<EPI, 256, 128, 4, 3, 64, 8>(a, s);

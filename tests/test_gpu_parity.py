@@ -254,11 +254,13 @@ def test_two_layer_full_shape(name):
     release(ver, W_dev)
 
 
-@pytest.mark.parametrize("batch,budget", [(1, 1), (4, 8), (4, 16), (16, 4), (1, 64)])
+@pytest.mark.parametrize("batch,budget", [(1, 1), (4, 1), (4, 4), (4, 8), (4, 16), (16, 4), (1, 64)])
 def test_two_layer_few_rows(batch, budget):
-    """8B shapes with 1 to 64 node rows: the skinny GEMM tiles (32 and 64
-    rows by 256 weight rows) and their K splits on every projection; a
-    64-node tree (256 query rows per KV head) takes the 8-wave attention."""
+    """8B shapes with 1 to 64 node rows: the few-rows products (up to 4 rows
+    for q/k/v and gate/up, up to 16 for the residual products, whose
+    RMSNorm then runs on its own), the 32- and 64-row GEMM tiles with their
+    K splits, and a 64-node tree (256 query rows per KV head) on the 8-wave
+    attention."""
     w = shallow(wl.sweep_workload(batch, budget))
     say(f"{w.name}: 2-layer 8B-shape model, {w.n_tokens} nodes")
     W_dev = wl.make_weights(w.cfg, 60 + budget, device="cuda")
