@@ -88,29 +88,67 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // out = bf16(x / sqrt(mean(x^2) + eps) * gain), one 256-thread block per row.
+// CPT > 0: the row is CPT 4-float chunks per thread (hidden <= 1024 * CPT),
+// all loaded (with their gains) before any is used, so a short row costs one
+// memory round trip (with few rows there are few blocks to hide latency);
+// CPT = 0: any length, a strided loop.  Both sum each thread's chunks in
+// column order, then the lanes, then the four waves: the same result.
+template <int CPT>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* x, const bf16* gain, bf16* out,
                                                       int hidden, float eps) {
   __shared__ float red[4];
   const int row = blockIdx.x;
   const float* xr = x + (size_t)row * hidden;
-  float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < hidden; c += 256 * 4) {
-    const f32x4 v = *(const f32x4*)(xr + c);
-    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
-  }
-  ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
-  const float rstd = rsqrtf(tot / (float)hidden + eps);
   bf16* orow = out + (size_t)row * hidden;
-  for (int c = threadIdx.x * 4; c < hidden; c += 256 * 4) {
-    const f32x4 v = *(const f32x4*)(xr + c);
-    const bf16x4 g = *(const bf16x4*)(gain + c);
-    bf16x4 y;
+  float ss = 0.f;
+  if constexpr (CPT > 0) {
+    f32x4 v[CPT];
+    bf16x4 g[CPT];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) y[k] = (bf16)(v[k] * rstd * (float)g[k]);
-    *(bf16x4*)(orow + c) = y;
+    for (int k = 0; k < CPT; ++k) {
+      const int c = (threadIdx.x + 256 * k) * 4;
+      if (c < hidden) {
+        v[k] = *(const f32x4*)(xr + c);
+        g[k] = *(const bf16x4*)(gain + c);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < CPT; ++k)
+      if ((threadIdx.x + 256 * k) * 4 < hidden)
+        ss += v[k][0] * v[k][0] + v[k][1] * v[k][1] + v[k][2] * v[k][2] + v[k][3] * v[k][3];
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float tot = red[0] + red[1] + red[2] + red[3];
+    const float rstd = rsqrtf(tot / (float)hidden + eps);
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int c = (threadIdx.x + 256 * k) * 4;
+      if (c < hidden) {
+        bf16x4 y;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) y[j] = (bf16)(v[k][j] * rstd * (float)g[k][j]);
+        *(bf16x4*)(orow + c) = y;
+      }
+    }
+  } else {
+    for (int c = threadIdx.x * 4; c < hidden; c += 256 * 4) {
+      const f32x4 v = *(const f32x4*)(xr + c);
+      ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float tot = red[0] + red[1] + red[2] + red[3];
+    const float rstd = rsqrtf(tot / (float)hidden + eps);
+    for (int c = threadIdx.x * 4; c < hidden; c += 256 * 4) {
+      const f32x4 v = *(const f32x4*)(xr + c);
+      const bf16x4 g = *(const bf16x4*)(gain + c);
+      bf16x4 y;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) y[k] = (bf16)(v[k] * rstd * (float)g[k]);
+      *(bf16x4*)(orow + c) = y;
+    }
   }
 }
 
@@ -250,7 +288,15 @@ hipError_t launch_embed(const int32_t* tokens, const bf16* table, float* x, int 
 
 hipError_t launch_rmsnorm(const float* x, const bf16* gain, bf16* out, int n, int hidden,
                           float eps, hipStream_t s) {
-  rmsnorm_kernel<<<n, 256, 0, s>>>(x, gain, out, hidden, eps);
+  switch ((hidden + 1023) / 1024) {
+    case 1: rmsnorm_kernel<1><<<n, 256, 0, s>>>(x, gain, out, hidden, eps); break;
+    case 2: rmsnorm_kernel<2><<<n, 256, 0, s>>>(x, gain, out, hidden, eps); break;
+    case 3:
+    case 4: rmsnorm_kernel<4><<<n, 256, 0, s>>>(x, gain, out, hidden, eps); break;
+    case 5: case 6: case 7:
+    case 8: rmsnorm_kernel<8><<<n, 256, 0, s>>>(x, gain, out, hidden, eps); break;
+    default: rmsnorm_kernel<0><<<n, 256, 0, s>>>(x, gain, out, hidden, eps); break;
+  }
   return hipGetLastError();
 }
 

@@ -167,6 +167,56 @@ def test_tiny_large_trees_and_commit():
     release(ver, W_dev)
 
 
+def random_gains(W, seed):
+    """Norm gains 1 + 0.25 N(0, 1), a different vector for every norm of
+    every layer (the generator's gains are all 1, which would hide a gain
+    applied to the wrong column or taken from the wrong norm)."""
+    g = torch.Generator().manual_seed(seed)
+
+    def r(t):
+        return (1.0 + 0.25 * torch.randn(t.shape, generator=g)).to(t.dtype)
+    W["final_norm"] = r(W["final_norm"])
+    for lw in W["layers"]:
+        lw["attn_norm"] = r(lw["attn_norm"])
+        lw["ffn_norm"] = r(lw["ffn_norm"])
+    return W
+
+
+@pytest.mark.parametrize("hidden,layers", [(256, 2), (6144, 1), (8320, 1)])
+def test_norm_gains_and_row_lengths(hidden, layers):
+    """Non-unit RMSNorm gains, and hidden sizes whose norm rows take each form
+    of the norm kernels: one 4-float chunk per thread (256), eight (6144) and
+    the strided loop past 8192 columns (8320, where the split-K reduction also
+    leaves the norm to the separate kernel).  Per model, a call of 5 rows (the
+    few-rows products, each followed by the separate norm) and one of 68 rows
+    (tile products)."""
+    base = wl.TINY
+    cfg = dataclasses.replace(base, n_layers=layers, hidden=hidden) if hidden == base.hidden else \
+        dataclasses.replace(base, n_layers=layers, hidden=hidden, head_dim=128, ffn=512)
+    say(f"norm gains: hidden {hidden}, {layers} layer(s)")
+    W_cpu = random_gains(wl.make_weights(cfg, 40 + hidden, dtype=torch.bfloat16), hidden)
+    W_dev = {"tok_embed": W_cpu["tok_embed"].cuda(), "final_norm": W_cpu["final_norm"].cuda(),
+             "lm_head": W_cpu["lm_head"].cuda(),
+             "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
+    rng = np.random.default_rng(hidden)
+    lens = [70, 0, 33, 120, 9]
+    caps = [S + 32 for S in lens]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=5, max_tokens=68)
+    gen = torch.Generator(device="cuda").manual_seed(hidden)
+    for i, S in enumerate(lens):
+        k, v = ver.kv.sample_view(i)
+        wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    few = [(wl.random_tokens(rng, 1, cfg.vocab), [-1]),
+           (wl.random_tokens(rng, 4, cfg.vocab), [-1, 0, 0, 1])]
+    full_check(cfg, W_cpu, ver, [1, 3], few, [lens[1], lens[3]], envelope=True)
+    many = [(wl.random_tokens(rng, 24, cfg.vocab), wl.recursive_tree(rng, 24, 6, 3)),
+            (wl.random_tokens(rng, 24, cfg.vocab), wl.recursive_tree(rng, 24, 5, 4)),
+            (wl.random_tokens(rng, 20, cfg.vocab), wl.chain_tree(20))]
+    full_check(cfg, W_cpu, ver, [0, 2, 4], many, [lens[0], lens[2], lens[4]], envelope=True)
+    release(ver, W_dev)
+
+
 def test_tiny_repeat_is_bitwise_identical():
     say("tiny repeatability")
     cfg, w, W_cpu, W_dev, ver = tiny_setup(5)
