@@ -46,7 +46,7 @@ constexpr size_t kAlign = 256;
 constexpr int kPartCap = 8192;          // split-KV partial tiles per call
 constexpr int kTargetSlots = 512;       // attention CU slots aimed for (two rounds of 256 CUs)
 constexpr int kMinChunk = 64;           // keys per split, lower bound
-constexpr int kSmallChunk = 256;        // below this, chunks are multiples of 64 keys
+constexpr int kSmallChunk = 256;        // small calls: chunks of 64-key multiples up to this
 constexpr int kMaxSplits = 64;          // key ranges per row tile (combine kernel's table)
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -408,14 +408,21 @@ int verify_impl(const spec_model_config* cfg, const spec_weights* w, spec_kv* kv
     }
     return slots;
   };
-  // Chunk length: a multiple of 128 keys, or of 64 when the whole call has
-  // under 256 keys' worth of work per slot (a single sample or a few short
-  // ones: more, shorter chunks shorten each work-group's serial block chain;
-  // measured at batch 1 with 1.1K keys, attention 0.50 -> 0.44 ms per 32-layer
-  // step against a 256-key floor).
+  // Chunk length: a multiple of 128 keys.  A small call (under kSmallChunk
+  // keys of work per slot at that target) instead aims at one round of the
+  // 256 CUs, in multiples of 64 keys between kMinChunk and kSmallChunk: a
+  // single short sample gets more, shorter chunks (each work-group's block
+  // chain is serial), and a few samples with multi-tile trees do not spill
+  // into a second round.  Measured per 32-layer step against a 256-key floor:
+  // batch 1, 1.1K keys, attention 0.50 -> 0.44 ms; against the two-round
+  // target at 64-key granularity: batch 4 x 16 nodes 5.75 -> 5.48 ms.
   auto round128 = [](int64_t x) { return (x + 127) / 128 * 128; };
-  const int64_t want = std::max<int64_t>((max_keys + kMaxSplits - 1) / kMaxSplits, (int64_t)(work / kTargetSlots));
-  int64_t chunk = want < kSmallChunk ? std::max<int64_t>(kMinChunk, (want + 63) / 64 * 64) : round128(want);
+  auto round64 = [](int64_t x) { return (x + 63) / 64 * 64; };
+  const int64_t min_split = (max_keys + kMaxSplits - 1) / kMaxSplits;
+  const int64_t want = std::max<int64_t>(min_split, (int64_t)(work / kTargetSlots));
+  int64_t chunk = round128(want);
+  if (want < kSmallChunk)
+    chunk = std::min<int64_t>(kSmallChunk, round64(std::max<int64_t>({kMinChunk, min_split, (int64_t)(work / 256)})));
   while (part_slots(chunk) > kPartCap) chunk += 128;    // terminates: one chunk per range has none
   // Work items.  Split key ranges write their partial states to per-tile
   // slots part + tile * ns + split.

@@ -153,16 +153,32 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* x, const bf16
 }
 
 // Row maximum over the LM-head partials; ties go to the lowest token id.
-__global__ __launch_bounds__(64) void argmax_reduce_kernel(const float* part_val,
-                                                           const int32_t* part_idx, int parts,
-                                                           int32_t* argmax, int32_t* dbg_argmax) {
+__global__ __launch_bounds__(256) void argmax_reduce_kernel(const float* part_val,
+                                                            const int32_t* part_idx, int parts,
+                                                            int32_t* argmax, int32_t* dbg_argmax) {
+  // (max, lowest index) is the same whatever order the partials are visited
+  // in, so each thread loads eight of them before comparing any: one memory
+  // round trip per 2048 partials instead of a dependent load per step.
+  constexpr int U = 8;
+  __shared__ float sv[4];
+  __shared__ int si[4];
   const int row = blockIdx.x;
+  const float* pvr = part_val + (size_t)row * parts;
+  const int32_t* pir = part_idx + (size_t)row * parts;
   float v = -INFINITY;
   int idx = 0x7fffffff;
-  for (int p = threadIdx.x; p < parts; p += 64) {
-    const float pv = part_val[(size_t)row * parts + p];
-    const int pi = part_idx[(size_t)row * parts + p];
-    if (pv > v || (pv == v && pi < idx)) { v = pv; idx = pi; }
+  for (int p0 = threadIdx.x; p0 < parts; p0 += 256 * U) {
+    float pv[U];
+    int pi[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int p = p0 + 256 * u;
+      pv[u] = p < parts ? pvr[p] : -INFINITY;
+      pi[u] = p < parts ? pir[p] : 0x7fffffff;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (pv[u] > v || (pv[u] == v && pi[u] < idx)) { v = pv[u]; idx = pi[u]; }
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
@@ -170,7 +186,12 @@ __global__ __launch_bounds__(64) void argmax_reduce_kernel(const float* part_val
     const int oi = __shfl_xor(idx, m);
     if (ov > v || (ov == v && oi < idx)) { v = ov; idx = oi; }
   }
+  if ((threadIdx.x & 63) == 0) { sv[threadIdx.x >> 6] = v; si[threadIdx.x >> 6] = idx; }
+  __syncthreads();
   if (threadIdx.x == 0) {
+#pragma unroll
+    for (int w = 1; w < 4; ++w)
+      if (sv[w] > v || (sv[w] == v && si[w] < idx)) { v = sv[w]; idx = si[w]; }
     if (idx == 0x7fffffff) idx = 0;   // every logit NaN: report token 0
     argmax[row] = idx;
     if (dbg_argmax) dbg_argmax[row] = idx;
@@ -302,7 +323,7 @@ hipError_t launch_rmsnorm(const float* x, const bf16* gain, bf16* out, int n, in
 
 hipError_t launch_argmax_reduce(const float* part_val, const int32_t* part_idx, int n, int parts,
                                 int32_t* argmax, int32_t* dbg_argmax, hipStream_t s) {
-  argmax_reduce_kernel<<<n, 64, 0, s>>>(part_val, part_idx, parts, argmax, dbg_argmax);
+  argmax_reduce_kernel<<<n, 256, 0, s>>>(part_val, part_idx, parts, argmax, dbg_argmax);
   return hipGetLastError();
 }
 
