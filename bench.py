@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 METRIC = "tree-verify tokens/s & accepted tokens/s, Llama-3-8B shape, 1 MI355X"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+FEW_ROWS_GATE_UP = 4           # gate/up rows up to which the library runs its few-rows kernel
 
 
 def parse():
@@ -539,10 +540,14 @@ def main():
                 "work_per_launch": f"2*{n_tok}*{2 * F}*{H} flop"}
     elif dominant == "gemm_gate_up":
         achieved = gu_bytes / (avg_ms / 1e3) / 1e9
+        # up to FEW_ROWS_GATE_UP rows the product runs the few-rows kernel
+        # (no K split leaves the work-group), otherwise the tile kernel
+        gu_kern = ("skinny_gemm_kernel<EPI_GATE_UP>" if n_tok <= FEW_ROWS_GATE_UP
+                   else "gemm_bf16_kernel<EPI_GATE_UP> (+ split-K reduce)")
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                 "traffic": recorded_traffic(args.workload, "gemm_bf16_kernel<EPI_GATE_UP>"),
-                "kernel": "gemm_bf16_kernel<EPI_GATE_UP> (+ split-K reduce)",
+                "kernel": gu_kern,
                 "work_per_launch": f"{gu_bytes} bytes (gate and up weights once, rows in and out)"}
     else:
         work = attention_work(cfg, w)
