@@ -10,7 +10,7 @@ Paper, Section 5:
   nodes (the root included, as in the paper's worked example where the
   root's weight is part of the sum);
 * t_sd (5.2): a regression on N_seq (summed committed lengths) and N_draft
-  (summed draft-token counts); this build adds the summed tree-size x
+  (summed draft-token counts); the library adds the summed tree-size x
   committed-length product as a third feature (the attention work that
   grows with both).  Bucket cache: feature values in one bucket share one
   prediction;

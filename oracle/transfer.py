@@ -18,7 +18,7 @@ Reading taken where the paper is silent:
 * within a layer, K precedes V; within a sample's part, the KV heads follow
   each other and each holds its tokens in order, head_dim values per token
   (the order of the cache itself);
-* this build holds one model (the target LLM); the draft model's part of
+* the library holds one model (the target LLM); the draft model's part of
   the hierarchy is empty.
 
 A sample's cache is given as two tensors ``k``, ``v`` of shape
