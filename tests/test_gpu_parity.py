@@ -217,6 +217,37 @@ def test_norm_gains_and_row_lengths(hidden, layers):
     release(ver, W_dev)
 
 
+@pytest.mark.parametrize("n_heads,n_kv,head_dim", [(4, 4, 64), (16, 2, 64), (4, 4, 128), (8, 1, 128)])
+def test_head_groups(n_heads, n_kv, head_dim):
+    """Query heads per KV head G = 1 (no sharing) and G = 8 (16 over 2 KV
+    heads at head dim 64, 8 over one at 128):
+    attention rows are node x G + head, so G sets how trees fill 32-row tiles
+    (a 64-node tree at G = 8 is 512 rows per KV head: the 8-wave kernel
+    over two 256-row groups) and which query head each row belongs to.
+    Ragged trees, one empty prefix, at head dims 64 and 128."""
+    cfg = dataclasses.replace(wl.TINY, n_heads=n_heads, n_kv_heads=n_kv, head_dim=head_dim)
+    say(f"head groups: {n_heads} q heads, {n_kv} kv heads, head_dim {head_dim}")
+    W_cpu = random_gains(wl.make_weights(cfg, 50 + n_heads + head_dim, dtype=torch.bfloat16), 7)
+    W_dev = {"tok_embed": W_cpu["tok_embed"].cuda(), "final_norm": W_cpu["final_norm"].cuda(),
+             "lm_head": W_cpu["lm_head"].cuda(),
+             "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
+    rng = np.random.default_rng(n_heads * 1000 + head_dim)
+    pars = [wl.recursive_tree(rng, 64, 8, 4), [-1], wl.chain_tree(9), wl.recursive_tree(rng, 33, 6, 3)]
+    lens = [150, 0, 61, 300]
+    caps = [S + len(p) + 8 for S, p in zip(lens, pars)]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=4, max_tokens=sum(len(p) for p in pars))
+    gen = torch.Generator(device="cuda").manual_seed(n_heads + head_dim)
+    ids = list(range(4))
+    for i, S in zip(ids, lens):
+        k, v = ver.kv.sample_view(i)
+        wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    trees = [(wl.random_tokens(rng, len(p), cfg.vocab), p) for p in pars]
+    out, r, exc = full_check(cfg, W_cpu, ver, ids, trees, lens)
+    check_tree_kv(cfg, ver, ids, trees, lens, r, ids)
+    release(ver, W_dev)
+
+
 def test_tiny_repeat_is_bitwise_identical():
     say("tiny repeatability")
     cfg, w, W_cpu, W_dev, ver = tiny_setup(5)
