@@ -248,6 +248,38 @@ def test_head_groups(n_heads, n_kv, head_dim):
     release(ver, W_dev)
 
 
+def test_widths_off_256():
+    """Widths that are multiples of 128 but not 256 (hidden 384, q segment
+    384, K/V segments 128, vocabulary 1152), so the tile choice falls back to
+    the 128-wide tiles for q/k/v, the residual products and the LM head (and
+    the LM head's partial count follows): a call of 4 rows (few-rows
+    products) and one of 74 rows."""
+    cfg = dataclasses.replace(wl.TINY, hidden=384, n_heads=6, n_kv_heads=2, head_dim=64, ffn=640,
+                              vocab=1152)
+    say("widths off 256: hidden 384, vocabulary 1152")
+    W_cpu = random_gains(wl.make_weights(cfg, 61, dtype=torch.bfloat16), 8)
+    W_dev = {"tok_embed": W_cpu["tok_embed"].cuda(), "final_norm": W_cpu["final_norm"].cuda(),
+             "lm_head": W_cpu["lm_head"].cuda(),
+             "layers": [{k: v.cuda() for k, v in lw.items()} for lw in W_cpu["layers"]]}
+    rng = np.random.default_rng(61)
+    lens = [90, 17, 0, 200]
+    caps = [S + 48 for S in lens]
+    ver = sv.Verifier(cfg, W_dev, caps, max_batch=4, max_tokens=74)
+    gen = torch.Generator(device="cuda").manual_seed(61)
+    for i, S in enumerate(lens):
+        k, v = ver.kv.sample_view(i)
+        wl.fill_prefix_kv(k, v, S, wl.prefix_kv_std(cfg), gen)
+    torch.cuda.synchronize()
+    few = [(wl.random_tokens(rng, 3, cfg.vocab), [-1, 0, 0]), (wl.random_tokens(rng, 1, cfg.vocab), [-1])]
+    out, r, exc = full_check(cfg, W_cpu, ver, [1, 2], few, [lens[1], lens[2]])
+    check_tree_kv(cfg, ver, [1, 2], few, [lens[1], lens[2]], r, [0, 1])
+    many = [(wl.random_tokens(rng, 40, cfg.vocab), wl.recursive_tree(rng, 40, 7, 3)),
+            (wl.random_tokens(rng, 34, cfg.vocab), wl.chain_tree(34))]
+    out, r, exc = full_check(cfg, W_cpu, ver, [0, 3], many, [lens[0], lens[3]])
+    check_tree_kv(cfg, ver, [0, 3], many, [lens[0], lens[3]], r, [0, 1])
+    release(ver, W_dev)
+
+
 def test_tiny_repeat_is_bitwise_identical():
     say("tiny repeatability")
     cfg, w, W_cpu, W_dev, ver = tiny_setup(5)
